@@ -1,0 +1,214 @@
+"""Benchmark of the 1xN-pruned convolution forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c1] [--no-cpu]
+
+A step is one forward pass of the workload's pruned layer(s) (Eq. 8 on the
+GPU) over one batch of synthetic input already resident in HBM.  Mask
+building and packing are the offline part of the method (done once per layer
+before deployment) and run before the timed region.  To keep timed steps from
+hitting the 256 MB Infinity Cache with the previous step's data, the input and
+output buffers rotate over enough copies to exceed 512 MB.
+
+Prints one JSON line.  value = actual TFLOP/s (2 * pixels * N * kh * kw * t
+per layer, summed) over the timed steps; the dense-equivalent rate and the
+HBM rate are reported beside it.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2105_14713_amd as onexn  # noqa: E402
+import workloads  # noqa: E402
+
+PEAK_HBM_GBPS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
+METRIC = "1×N sparse conv fwd: actual & dense-equiv TFLOP/s, % of MFMA/HBM roofline"
+ROTATE_BYTES = 512 << 20
+
+WORKLOADS = {
+    "c0": workloads.config0,
+    "c1": workloads.config1,
+    "c2": workloads.config2,
+    "c4": lambda: workloads.config4("bf16"),
+    "c4f32": lambda: workloads.config4("f32"),
+}
+for _N in (4, 8, 16, 32):
+    for _p in (0.3, 0.5, 0.7):
+        WORKLOADS[f"c3_n{_N}_p{int(_p * 100)}"] = (lambda N=_N, p=_p: workloads.config3(N, p))
+
+_ESIZE = {"f32": 4, "bf16": 2}
+_TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def layer_work(layer, packed, batch, dtype, out_dtype):
+    """Algorithmic flops and HBM bytes of one forward of one layer."""
+    px = layer.out_pixels(batch)
+    kk = layer.k * layer.k
+    f_act = 2.0 * px * layer.N * kk * packed.t
+    f_dense = 2.0 * px * layer.cout * layer.cin * kk
+    used_ch = int((packed.mask.sum(dim=1) > 0).sum())
+    e = _ESIZE[dtype]
+    b_x = batch * layer.H * layer.H * used_ch * e
+    b_y = px * layer.cout * _ESIZE[out_dtype]
+    b_w = packed.t * layer.N * kk * e + packed.t * 4 + (packed.P.numel()) * 4
+    return f_act, f_dense, b_x + b_y + b_w
+
+
+def cpu_baseline(layers, batch, wl, budget_s):
+    """The oracle (direct 7-loop over the masked dense weight, fp64) on the host
+    cores, over a bounded sample: whole images of the workload's layers, taken
+    in order until the time budget is spent."""
+    import oracle
+    done_f, spent, imgs = 0.0, 0.0, 0
+    lw = []
+    for layer in layers:
+        w, x = workloads.gen_layer(layer, 1, wl.dtype)
+        pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+        lw.append((layer, pr, x.double().numpy()))
+    for b in range(batch):
+        for layer, pr, x in lw:
+            t0 = time.perf_counter()
+            oracle.conv2d(x, pr.wbar, (layer.stride,) * 2, (layer.pad,) * 2)
+            spent += time.perf_counter() - t0
+            done_f += 2.0 * layer.Ho * layer.Ho * layer.N * layer.k * layer.k * pr.t
+        imgs += 1
+        if spent >= budget_s:
+            break
+    return {"value": done_f / spent / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{imgs} of {batch} images through all {len(layers)} layer(s): fp64 direct "
+                      f"convolution over the masked dense weight, {spent:.1f} s; rate counts the "
+                      f"1xN kernel's actual flops"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c1", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--traffic", default=None,
+                    help="HBM bytes per launch measured by rocprofv3 (FETCH+WRITE, scaled)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the 1xN conv path here is single-GPU "
+              "(multi-GPU sharding is a design note, not built); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = WORKLOADS[args.workload]()
+    batch = wl.batch
+    odt = _TDT[wl.out_dtype]
+
+    # Offline: generate, build masks, pack, copy to the device.
+    prepared = []
+    f_act = f_dense = b_alg = 0.0
+    t_host = 0.0
+    for layer in wl.layers:
+        w, x = workloads.gen_layer(layer, batch, wl.dtype)
+        t0 = time.perf_counter()
+        packed = onexn.prepare_layer(w, layer.N, layer.p, layer.rearrange, dev)
+        t_host += time.perf_counter() - t0
+        fa, fd, bb = layer_work(layer, packed, batch, wl.dtype, wl.out_dtype)
+        f_act, f_dense, b_alg = f_act + fa, f_dense + fd, b_alg + bb
+        xd = x.to(dev)
+        Ho = layer.Ho
+        copies = max(1, math.ceil(ROTATE_BYTES / max(bb, 1)))
+        copies = min(copies, 16)
+        xs = [xd] + [xd.clone() for _ in range(copies - 1)]
+        ys = [torch.empty((batch, layer.cout, Ho, Ho), dtype=odt, device=dev) for _ in range(copies)]
+        prepared.append((layer, packed, xs, ys))
+        del x, w
+
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        for layer, packed, xs, ys in prepared:
+            r = i % len(xs)
+            packed.forward(xs[r], layer.stride, layer.pad, "nchw", odt, out=ys[r],
+                           stream=stream.cuda_stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # Timed region: K steps, events around every step on the launch stream.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record(stream)
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(args.warmup + i)
+        ev[i][1].record(stream)
+    t_all1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_all0.elapsed_time(t_all1)
+    per_step = sorted(a.elapsed_time(b) for a, b in ev)
+    avg_step_ms = sum(per_step) / len(per_step)
+    ms_per_step = total_ms / args.steps
+
+    dtype = wl.dtype
+    peak = PEAK_TFLOPS[dtype]
+    t_compute = f_act / (peak * 1e12)
+    t_hbm = b_alg / (PEAK_HBM_GBPS * 1e9)
+    bound = "mfma" if t_compute >= t_hbm else "hbm"
+    avg_s = avg_step_ms / 1e3
+    if bound == "mfma":
+        achieved, pk, unit = f_act / avg_s / 1e12, peak, "TFLOP/s"
+    else:
+        achieved, pk, unit = b_alg / avg_s / 1e9, PEAK_HBM_GBPS, "GB/s"
+    traffic = float(args.traffic) if args.traffic else None
+
+    rec = {
+        "metric": METRIC,
+        "value": round(f_act * args.steps / (total_ms / 1e3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "batch": batch,
+                   "layers": len(wl.layers), "out_dtype": wl.out_dtype, "layout": "nchw"},
+        "dense_equiv_tflops": round(f_dense * args.steps / (total_ms / 1e3) / 1e12, 3),
+        "hbm_gbps": round(b_alg * args.steps / (total_ms / 1e3) / 1e9, 1),
+        "kernel_us": {"mean": round(avg_step_ms * 1e3, 2), "p10": round(per_step[len(per_step) // 10] * 1e3, 2),
+                      "p50": round(per_step[len(per_step) // 2] * 1e3, 2),
+                      "p90": round(per_step[(9 * len(per_step)) // 10] * 1e3, 2)},
+        "flops_actual_per_step": f_act,
+        "flops_dense_per_step": f_dense,
+        "bytes_alg_per_step": b_alg,
+        "t_roof_us": round(max(t_compute, t_hbm) * 1e6, 2),
+        "frac_of_roofline": round(max(t_compute, t_hbm) / avg_s, 4),
+        "roofline": {"bound": bound, "achieved": round(achieved, 3), "peak": pk, "unit": unit,
+                     "frac": round(achieved / pk, 4), "traffic": traffic},
+        "host_prepare_s": round(t_host, 3),
+    }
+    if not args.no_cpu:
+        rec["cpu_baseline"] = cpu_baseline(wl.layers, batch, wl, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,141 @@
+/*
+ * onexn: 1xN-pruned convolution on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libonexn.so.  Plain pointers and sizes only.
+ *
+ * The method is 1xN pruning (Lin et al., "1xN Pattern for Pruning
+ * Convolutional Neural Networks", arXiv 2105.14713).  A layer's weight W has
+ * shape [n][m][kh][kw] (n output channels, m input channels; Sec. 3.1).  Seen
+ * as the m x n matrix Omega of kh x kw kernels (Sec. 3.2), each row is cut
+ * into G = ceil(n/N) col-groups of N consecutive output kernels; one such
+ * 1xN block is the pruning unit.  The last col-group is ragged when N does
+ * not divide n: its rows at and beyond n do not exist (they score 0 and are
+ * stored as 0).
+ *
+ * Common conventions
+ *   - Weights are OIHW, row-major: w[((j*m + k)*kh + q)*kw + r].
+ *   - bf16 values are raw IEEE bfloat16 bit patterns in uint16_t.
+ *   - The caller owns every buffer.  No function keeps a pointer after it
+ *     returns.  Host functions are re-entrant and thread-safe.
+ *   - On error nothing is written to the outputs of host functions, and the
+ *     conv call enqueues nothing.  onexn_last_error() gives a message for the
+ *     last failure on the calling thread.
+ */
+#ifndef ONEXN_H
+#define ONEXN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ONEXN_OK = 0,
+    ONEXN_ERR_NULL = 1,        /* a required pointer is NULL */
+    ONEXN_ERR_ARG = 2,         /* a scalar is out of range, or perm/mask/t are inconsistent */
+    ONEXN_ERR_SHAPE = 3,       /* sizes give an empty or overflowing output */
+    ONEXN_ERR_DTYPE = 4,       /* unknown dtype, or a dtype combination that is not allowed */
+    ONEXN_ERR_UNSUPPORTED = 5, /* valid request this build does not implement */
+    ONEXN_ERR_BUFSIZE = 6,     /* an index or size does not fit the int32 BSR arrays */
+    ONEXN_ERR_HIP = 7          /* the HIP runtime reported an error */
+} onexn_status;
+
+typedef enum { ONEXN_F32 = 0, ONEXN_BF16 = 1 } onexn_dtype;
+typedef enum { ONEXN_NCHW = 0, ONEXN_NHWC = 1 } onexn_layout;
+
+/*
+ * Mask building (host, synchronous).
+ *
+ * Does, in the paper's order:
+ *  1. Filter rearrangement (Sec. 3.3, Fig. 2): if `rearrange` is non-zero,
+ *     order the filters by decreasing l1 norm sum_{k,q,r} |W[j][k][q][r]|;
+ *     equal norms keep ascending original index.  perm[j'] = original index
+ *     of the filter at rearranged position j' (identity if rearrange == 0).
+ *     The caller applies the same permutation to the next layer's input
+ *     channels, W2[:, perm], and to any per-channel parameters of this layer.
+ *  2. Block scores (Sec. 3.2, Eq. 4-5): the l1 norm of each 1xN block of the
+ *     rearranged weights, summed in fp64 over block rows i < N, then q, r.
+ *  3. Per-layer top-(1-p) selection (Eq. 1, the solution of Eq. 5, Sec. 4.1):
+ *     of the K = m*G blocks, floor(p*K + 0.5) (clamped to [0, K]) are
+ *     pruned; the t = K - pruned blocks with the largest scores are kept,
+ *     equal scores keeping the lower row-major index k*G + g.
+ *
+ * w:     host [n][m][kh][kw] in wdt.
+ * N:     block length, 1 <= N; p: pruning rate in [0, 1].
+ * perm:  out, host int32[n].
+ * mask:  out, host uint8[m][G] (row-major by input channel k): 1 = kept.
+ * t:     out, number of kept blocks.
+ * Errors: NULL, DTYPE, ARG (non-positive size, N < 1, p not in [0,1]),
+ *         BUFSIZE (n*m*kh*kw or m*G beyond 2^31 - 1).
+ */
+onexn_status onexn_build_mask(const void* w, onexn_dtype wdt, int32_t n, int32_t m, int32_t kh,
+                              int32_t kw, int32_t N, double p, int32_t rearrange, int32_t* perm,
+                              uint8_t* mask, int64_t* t);
+
+/*
+ * BSR packing (host, synchronous): Sec. 3.4 and Fig. 3.
+ *
+ * Encodes Omega-bar = rearranged W masked by `mask` (Eq. 6) into
+ *   P: int32[G+1]   start of col-group g in D and I; P[0] = 0, P[G] = t
+ *                   (0-based; the paper's P is 1-based with last entry t+1);
+ *   I: int32[t]     input channel k of each stored block, ascending within
+ *                   a col-group;
+ *   D: [t][N][kh][kw] in wdt, block z = the kernels of output channels
+ *                   gN .. gN+N-1 (rearranged order) for input channel I[z];
+ *                   rows at and beyond n are 0.
+ * perm and mask are the outputs of onexn_build_mask (any permutation and any
+ * 0/1 mask are accepted); t must equal the number of ones in mask.
+ * Errors: NULL, DTYPE, ARG (perm not a permutation of 0..n-1, mask entry not
+ *         0/1, t inconsistent), BUFSIZE.
+ */
+onexn_status onexn_pack(const void* w, onexn_dtype wdt, int32_t n, int32_t m, int32_t kh,
+                        int32_t kw, int32_t N, const int32_t* perm, const uint8_t* mask,
+                        int64_t t, int32_t* P, int32_t* I, void* D);
+
+/*
+ * Forward convolution of a 1xN-pruned layer (device, asynchronous).
+ *
+ * Computes the block-wise decode of Eq. 8, which equals the dense product of
+ * Eq. 7 with Omega-bar: for every output pixel and col-group g,
+ *   Y[pixel][gN .. gN+N-1] = sum_{z=P[g]}^{P[g+1]-1} X[pixel, I[z]] . D[z]
+ * where for a kh x kw kernel X[pixel, c] is the input patch of channel c under
+ * the output pixel (stride, zero padding) and "." the patch-kernel inner
+ * product.  Output channels are in rearranged order (no un-permute).
+ * Accumulation is fp32.
+ *
+ * P_dev, I_dev, D_dev: device BSR arrays from onexn_pack (G+1, t, t*N*kh*kw
+ *         entries).  Entries of I outside [0, m) are skipped and P is clamped
+ *         to [0, t], so malformed arrays cannot cause out-of-bounds reads.
+ * x_dev:  device input [batch][m][H][W] (NCHW) or [batch][H][W][m] (NHWC).
+ * y_dev:  device output [batch][n][Ho][Wo] or [batch][Ho][Wo][n] (same layout
+ *         as x), Ho = (H + 2*pad_h - kh)/stride_h + 1, likewise Wo.  Every
+ *         element is written.  y must not overlap x, P, I or D.
+ * dtypes: wdt == xdt (F32 or BF16); ydt == xdt or F32.
+ * stream: hipStream_t to enqueue on (NULL = the null stream).  The call
+ *         validates its arguments, launches, and returns without waiting.
+ * Supported: N in {1, 2, 4, 8, 16, 32}; 1 <= kh, kw <= 16; stride 1..8;
+ *         0 <= pad < 16; m*H*W and n*Ho*Wo below 2^31 (per image).
+ * Errors: NULL, DTYPE, ARG, SHAPE (Ho or Wo < 1), UNSUPPORTED, HIP (launch
+ *         failed).  batch == 0 is a no-op after the checks; x and y may then
+ *         be NULL.
+ */
+onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                              onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw,
+                              int32_t N, int64_t t, const void* x_dev, onexn_dtype xdt,
+                              onexn_layout layout, int32_t batch, int32_t H, int32_t W,
+                              int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                              void* y_dev, onexn_dtype ydt, void* stream);
+
+/* Static name of a status code ("ONEXN_OK", ...); "ONEXN_UNKNOWN" otherwise. */
+const char* onexn_status_string(onexn_status s);
+
+/* Message describing the last error on the calling thread ("" if none).
+ * The pointer stays valid until the next onexn call on the same thread. */
+const char* onexn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ONEXN_H */

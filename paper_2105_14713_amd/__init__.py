@@ -1,0 +1,214 @@
+"""onexn: 1xN-pruned convolution on AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding of ``libonexn.so`` (C ABI in ``include/onexn.h``).  The
+functions here only marshal arguments: mask building and packing run in the
+library's host C++, the convolution runs in its HIP kernels.  torch is used
+for host/device memory and for the current HIP stream.  There is no fallback:
+if the library is missing every call raises.
+
+    perm, mask, t = build_mask(w, N, p, rearrange)        # Sec. 3.2-3.3, Eq. 1/5
+    P, I, D = pack(w, N, perm, mask, t)                     # Sec. 3.4, Fig. 3
+    y = conv2d_fwd(P, I, D, n, x, N, stride, pad)           # Eq. 8 on the GPU
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libonexn.so")
+
+ONEXN_OK = 0
+_STATUS_NAMES = ["ONEXN_OK", "ONEXN_ERR_NULL", "ONEXN_ERR_ARG", "ONEXN_ERR_SHAPE",
+                 "ONEXN_ERR_DTYPE", "ONEXN_ERR_UNSUPPORTED", "ONEXN_ERR_BUFSIZE", "ONEXN_ERR_HIP"]
+F32, BF16 = 0, 1
+NCHW, NHWC = 0, 1
+
+EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_status_string",
+            "onexn_last_error")
+
+_lib = None
+
+
+class OnexnError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        self.status = status
+        name = _STATUS_NAMES[status] if 0 <= status < len(_STATUS_NAMES) else str(status)
+        super().__init__(f"{where}: {name}: {message}")
+
+
+def load_library():
+    """Loads libonexn.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2105_14713_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    c_i32, c_i64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    lib.onexn_build_mask.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                     ctypes.c_double, c_i32, c_vp, c_vp, c_vp]
+    lib.onexn_build_mask.restype = ctypes.c_int
+    lib.onexn_pack.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp,
+                               c_i64, c_vp, c_vp, c_vp]
+    lib.onexn_pack.restype = ctypes.c_int
+    lib.onexn_conv2d_fwd.argtypes = ([c_vp, c_vp, c_vp, ctypes.c_int] + [c_i32] * 5 + [c_i64] +
+                                     [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
+                                     [c_vp, ctypes.c_int, c_vp])
+    lib.onexn_conv2d_fwd.restype = ctypes.c_int
+    lib.onexn_status_string.argtypes = [ctypes.c_int]
+    lib.onexn_status_string.restype = ctypes.c_char_p
+    lib.onexn_last_error.argtypes = []
+    lib.onexn_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().onexn_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return load_library().onexn_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != ONEXN_OK:
+        raise OnexnError(status, where, last_error())
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {dt}; expected float32 or bfloat16")
+
+
+def _host_weight(w: torch.Tensor) -> torch.Tensor:
+    if w.dim() != 4:
+        raise ValueError("weight must be [n][m][kh][kw]")
+    if w.device.type != "cpu":
+        raise ValueError("mask building and packing take a host (CPU) weight tensor")
+    return w.contiguous()
+
+
+def build_mask(w: torch.Tensor, N: int, p: float, rearrange: bool) -> Tuple[torch.Tensor, torch.Tensor, int]:
+    """``onexn_build_mask``: returns (perm int32[n], mask uint8[m][G], t)."""
+    w = _host_weight(w)
+    n, m, kh, kw = w.shape
+    G = -(-n // int(N)) if N > 0 else 1
+    perm = torch.empty(n, dtype=torch.int32)
+    mask = torch.empty((m, G), dtype=torch.uint8)
+    t = ctypes.c_int64(0)
+    st = load_library().onexn_build_mask(w.data_ptr(), _dtype_code(w.dtype), n, m, kh, kw, int(N),
+                                         float(p), int(bool(rearrange)), perm.data_ptr(),
+                                         mask.data_ptr(), ctypes.addressof(t))
+    _check(st, "onexn_build_mask")
+    return perm, mask, int(t.value)
+
+
+def pack(w: torch.Tensor, N: int, perm: torch.Tensor, mask: torch.Tensor, t: int):
+    """``onexn_pack``: returns host (P int32[G+1], I int32[t], D [t][N][kh][kw] in w's dtype)."""
+    w = _host_weight(w)
+    n, m, kh, kw = w.shape
+    G = -(-n // int(N))
+    perm = perm.to(torch.int32).contiguous()
+    mask = mask.to(torch.uint8).contiguous()
+    if perm.numel() != n or mask.numel() != m * G:
+        raise ValueError("perm/mask sizes do not match the weight and N")
+    P = torch.empty(G + 1, dtype=torch.int32)
+    I = torch.empty(max(int(t), 1), dtype=torch.int32)
+    D = torch.empty((max(int(t), 1), int(N), kh, kw), dtype=w.dtype)
+    st = load_library().onexn_pack(w.data_ptr(), _dtype_code(w.dtype), n, m, kh, kw, int(N),
+                                   perm.data_ptr(), mask.data_ptr(), int(t), P.data_ptr(),
+                                   I.data_ptr(), D.data_ptr())
+    _check(st, "onexn_pack")
+    return P, I[:int(t)], D[:int(t)]
+
+
+def out_hw(H: int, W: int, kh: int, kw: int, stride, pad) -> Tuple[int, int]:
+    return (H + 2 * pad[0] - kh) // stride[0] + 1, (W + 2 * pad[1] - kw) // stride[1] + 1
+
+
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
+               stride=1, pad=0, layout: str = "nchw", out_dtype: Optional[torch.dtype] = None,
+               out: Optional[torch.Tensor] = None, stream: Optional[int] = None) -> torch.Tensor:
+    """``onexn_conv2d_fwd`` on device tensors; enqueued on ``stream`` (default:
+    torch's current stream), no synchronisation.  Returns y (rearranged channel order)."""
+    for name, tns in (("P", P), ("I", I), ("D", D), ("x", x)):
+        if tns.device.type != "cuda":
+            raise ValueError(f"{name} must be a device tensor (the convolution only runs on the GPU)")
+        if not tns.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if D.dim() != 4:
+        raise ValueError("D must be [t][N][kh][kw]")
+    t, N, kh, kw = D.shape
+    if t != I.numel():
+        raise ValueError("D and I disagree on t")
+    lay = {"nchw": NCHW, "nhwc": NHWC}[layout]
+    if lay == NCHW:
+        B, m, H, W = x.shape
+    else:
+        B, H, W, m = x.shape
+    stride, pad = _pair(stride), _pair(pad)
+    Ho, Wo = out_hw(H, W, kh, kw, stride, pad)
+    odt = x.dtype if out_dtype is None else out_dtype
+    shape = (B, n, Ho, Wo) if lay == NCHW else (B, Ho, Wo, n)
+    if out is None:
+        out = torch.empty(shape, dtype=odt, device=x.device)
+    elif tuple(out.shape) != shape or out.dtype != odt or not out.is_contiguous():
+        raise ValueError("out has the wrong shape, dtype or layout")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device).cuda_stream
+    st = load_library().onexn_conv2d_fwd(
+        P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype),
+        int(n), m, kh, kw, N, t, x.data_ptr(), _dtype_code(x.dtype), lay, B, H, W, stride[0],
+        stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt), stream)
+    _check(st, "onexn_conv2d_fwd")
+    return out
+
+
+@dataclass
+class PackedLayer:
+    """A pruned layer's BSR arrays resident on the device plus its metadata."""
+    n: int
+    m: int
+    kh: int
+    kw: int
+    N: int
+    t: int
+    perm: torch.Tensor   # host int32[n]
+    mask: torch.Tensor   # host uint8[m][G]
+    P: torch.Tensor      # device int32[G+1]
+    I: torch.Tensor      # device int32[t]
+    D: torch.Tensor      # device [t][N][kh][kw]
+
+    def forward(self, x, stride=1, pad=0, layout="nchw", out_dtype=None, out=None, stream=None):
+        return conv2d_fwd(self.P, self.I, self.D, self.n, x, stride, pad, layout, out_dtype, out,
+                          stream)
+
+
+def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
+                  device="cuda") -> PackedLayer:
+    """Offline steps (mask, pack) on the host, then one copy of P, I, D to the device."""
+    perm, mask, t = build_mask(w, N, p, rearrange)
+    P, I, D = pack(w, N, perm, mask, t)
+    n, m, kh, kw = w.shape
+    dev = torch.device(device)
+    if t == 0:   # keep valid device allocations even with nothing kept
+        I = torch.zeros(1, dtype=torch.int32)[:0]
+        D = torch.zeros((0, N, kh, kw), dtype=w.dtype)
+    return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
+
+
+__all__ = ["BF16", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
+           "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
+           "prepare_layer", "status_string"]

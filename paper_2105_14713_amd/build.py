@@ -1,0 +1,45 @@
+"""Builds libonexn.so (HIP kernels for gfx950 + host C++) in-tree.
+
+    python -m paper_2105_14713_amd.build
+
+hipcc cross-compiles for gfx950; no GPU is needed to build.
+"""
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INC = os.path.join(ROOT, "include")
+OUT = os.path.join(PKG, "_build")
+LIB = os.path.join(PKG, "libonexn.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+# Packed fp32 VALU ops are disabled for all device code (see the kernel notes).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I" + INC, "-I" + CSRC]
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(OUT, exist_ok=True)
+    host_o = os.path.join(OUT, "onexn_host.o")
+    conv_o = os.path.join(OUT, "onexn_conv.o")
+    _run(["g++"] + COMMON + ["-c", os.path.join(CSRC, "onexn_host.cpp"), "-o", host_o], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH] + COMMON + DEVICE_FLAGS +
+         ["-c", os.path.join(CSRC, "onexn_conv.hip"), "-o", conv_o], verbose)
+    tmp = LIB + ".tmp"
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", host_o, conv_o, "-o", tmp], verbose)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,251 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle.
+
+Bars: integer-valued inputs are bit-exact in fp32; fp32 inputs within
+max|y - ref| / max|ref| <= 1e-5; bf16 inputs (fp32 accumulation) within 2e-2
+for bf16 output (and 1e-5 for fp32 output, where only accumulation rounds),
+the oracle seeing the same bf16-rounded values.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2105_14713_amd as onexn
+import workloads
+from gpu_helpers import gpu_conv, oracle_conv, rel_err, sample_indices
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # (k, stride, pad)
+    (1, 1, 0), (1, 2, 0), (3, 1, 1), (3, 2, 1), (7, 2, 3), (3, 1, 0),
+]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lib = onexn.load_library()
+    assert os.path.samefile(lib._name, onexn.LIB_PATH)
+
+
+def _n_for(N):
+    # several col-groups with a ragged last one (none for N = 1)
+    return {1: 7, 2: 9, 4: 18, 8: 28, 16: 40, 32: 72}[N]
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+@pytest.mark.parametrize("kshape", SHAPES, ids=lambda s: f"k{s[0]}s{s[1]}p{s[2]}")
+@pytest.mark.parametrize("N", [1, 2, 4, 8, 16, 32])
+def test_integer_exact(N, kshape, layout):
+    k, s, pd = kshape
+    n = _n_for(N)
+    print(f"case N={N} k={k} s={s} pad={pd} layout={layout}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=10 * N + k, cout=n, cin=13, k=k, batch=3, H=19, W=17)
+    y, layer = gpu_conv(w, x, N, 0.5, True, s, pd, layout)
+    ref, pr = oracle_conv(w, x, N, 0.5, True, s, pd)
+    assert layer.t == pr.t
+    np.testing.assert_array_equal(y, ref)
+
+
+@pytest.mark.parametrize("kshape", SHAPES, ids=lambda s: f"k{s[0]}s{s[1]}p{s[2]}")
+@pytest.mark.parametrize("N", [4, 8, 16, 32])
+def test_float_fp32(N, kshape):
+    k, s, pd = kshape
+    gen = torch.Generator().manual_seed(N * 100 + k)
+    n, m = _n_for(N), 37
+    w = workloads.gen_weight(gen, n, m, k)
+    x = workloads.gen_activation(gen, (2, m, 23, 21))
+    y, _ = gpu_conv(w, x, N, 0.3, False, s, pd)
+    ref, _ = oracle_conv(w, x, N, 0.3, False, s, pd)
+    assert rel_err(y, ref) <= 1e-5
+
+
+@pytest.mark.parametrize("out_dtype", [torch.bfloat16, torch.float32], ids=["ybf16", "yf32"])
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+@pytest.mark.parametrize("kshape", [(1, 1, 0), (3, 1, 1), (3, 2, 1)], ids=lambda s: f"k{s[0]}s{s[1]}")
+@pytest.mark.parametrize("N", [4, 8, 16, 32])
+def test_bf16(N, kshape, layout, out_dtype):
+    k, s, pd = kshape
+    gen = torch.Generator().manual_seed(N + k)
+    n, m = _n_for(N), 45
+    w = workloads.gen_weight(gen, n, m, k).bfloat16()
+    x = workloads.gen_activation(gen, (2, m, 20, 19)).bfloat16()
+    y, _ = gpu_conv(w, x, N, 0.7, True, s, pd, layout, out_dtype)
+    ref, _ = oracle_conv(w, x, N, 0.7, True, s, pd)
+    err = rel_err(y, ref)
+    if out_dtype == torch.bfloat16:
+        assert err <= 2e-2
+        assert err <= 2.0 ** -8          # one bf16 rounding of the output
+    else:
+        assert err <= 1e-5
+
+
+def test_bf16_integer_exact():
+    """Small integers are exact in bf16, so bf16 -> fp32 output must be bit-exact."""
+    for N in (8, 16, 32):
+        w, x = workloads.gen_integer_layer(seed=N, cout=_n_for(N), cin=40, k=3, batch=2, H=14)
+        y, _ = gpu_conv(w.bfloat16(), x.bfloat16(), N, 0.5, False, 1, 1, "nchw", torch.float32)
+        ref, _ = oracle_conv(w, x, N, 0.5, False, 1, 1)
+        np.testing.assert_array_equal(y, ref)
+
+
+# ---------------------------------------------------------------------------
+# Edge cases.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("N", [4, 16, 32])
+def test_all_pruned_writes_zeros(N):
+    w, x = workloads.gen_integer_layer(seed=1, cout=40, cin=9, k=3, batch=2, H=10)
+    y, layer = gpu_conv(w, x, N, 1.0, True, 1, 1)      # output prefilled with NaN
+    assert layer.t == 0
+    assert np.all(y == 0.0)
+
+
+@pytest.mark.parametrize("N", [4, 8, 16, 32])
+def test_dense_p0_equals_library_conv(N):
+    gen = torch.Generator().manual_seed(3)
+    w = workloads.gen_weight(gen, 64, 24, 3)
+    x = workloads.gen_activation(gen, (2, 24, 15, 15))
+    y, layer = gpu_conv(w, x, N, 0.0, False, 1, 1)
+    ref = torch.nn.functional.conv2d(x.double(), w.double(), padding=1).numpy()
+    assert layer.t == 24 * (64 // N)
+    assert rel_err(y, ref) <= 1e-5
+
+
+def test_batch_zero_is_noop():
+    w, _ = workloads.gen_integer_layer(seed=2, cout=32, cin=8, k=1, batch=1, H=4)
+    layer = onexn.prepare_layer(w, 16, 0.5, False)
+    x = torch.zeros((0, 8, 4, 4), device="cuda")
+    y = layer.forward(x)
+    assert y.shape == (0, 32, 4, 4)
+
+
+@pytest.mark.parametrize("case", [
+    dict(n=32, m=5, k=1, N=32, B=1, H=1, s=1, pd=0),     # one col-group, one pixel
+    dict(n=16, m=3, k=1, N=16, B=1, H=3, s=2, pd=0),     # stride larger than the kernel
+    dict(n=8, m=2, k=3, N=4, B=1, H=2, s=1, pd=2),       # padding larger than the input
+    dict(n=33, m=600, k=3, N=32, B=1, H=6, s=1, pd=1),   # long contraction, 1-row last group
+    dict(n=100, m=17, k=1, N=4, B=5, H=13, s=1, pd=0),   # many groups, ragged pixel tail
+    dict(n=48, m=7, k=5, N=16, B=2, H=9, s=3, pd=2),     # 5x5, stride 3
+])
+def test_edge_shapes_integer_exact(case):
+    c = case
+    print(f"edge case {c}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=c["n"] + c["m"], cout=c["n"], cin=c["m"], k=c["k"],
+                                       batch=c["B"], H=c["H"], wmax=2, xmax=2)
+    y, _ = gpu_conv(w, x, c["N"], 0.5, True, c["s"], c["pd"])
+    ref, _ = oracle_conv(w, x, c["N"], 0.5, True, c["s"], c["pd"])
+    np.testing.assert_array_equal(y, ref)
+
+
+def test_malformed_bsr_is_safe():
+    """I entries outside [0, m) are skipped and P is clamped to [0, t]."""
+    w, x = workloads.gen_integer_layer(seed=4, cout=32, cin=6, k=1, batch=1, H=5)
+    layer = onexn.prepare_layer(w, 16, 0.5, False)
+    I = layer.I.clone()
+    I[0] = 1 << 20
+    P = layer.P.clone()
+    P[-1] = 1 << 30
+    y = onexn.conv2d_fwd(P, I, layer.D, 32, x.cuda())
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+
+
+def test_runs_on_a_side_stream():
+    w, x = workloads.gen_integer_layer(seed=5, cout=32, cin=6, k=3, batch=2, H=8)
+    layer = onexn.prepare_layer(w, 16, 0.5, False)
+    s = torch.cuda.Stream()
+    xd = x.cuda()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        y = layer.forward(xd, 1, 1)
+    s.synchronize()
+    ref, _ = oracle_conv(w, x, 16, 0.5, False, 1, 1)
+    np.testing.assert_array_equal(y.double().cpu().numpy(), ref)
+
+
+# ---------------------------------------------------------------------------
+# The benchmark workloads at full size (same entry point and launch
+# configuration as the benchmark), checked on sampled outputs.
+# ---------------------------------------------------------------------------
+
+def _check_sampled(layer, batch, dtype, out_dtype, y, pr, x_cpu, count=3000, seed=0):
+    idx = sample_indices(tuple(y.shape), count, seed, layer.N)
+    got = y.float().reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
+    ref = oracle.conv2d_at(x_cpu.double().numpy(), pr.wbar, idx, (layer.stride,) * 2,
+                           (layer.pad,) * 2)
+    err = rel_err(got, ref)
+    bar = 2e-2 if out_dtype == "bf16" else 1e-5
+    assert err <= bar, f"{layer.name}: rel err {err:.3g} > {bar}"
+    return err
+
+
+def _run_layer(layer, batch, dtype="f32", out_dtype="f32"):
+    w, x = workloads.gen_layer(layer, batch, dtype)
+    packed = onexn.prepare_layer(w, layer.N, layer.p, layer.rearrange)
+    odt = torch.bfloat16 if out_dtype == "bf16" else torch.float32
+    y = packed.forward(x.cuda(), layer.stride, layer.pad, "nchw", odt)
+    torch.cuda.synchronize()
+    pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+    assert packed.t == pr.t
+    return y, pr, x
+
+
+def test_config0_full():
+    wl = workloads.config0()
+    layer = wl.layers[0]
+    y, pr, x = _run_layer(layer, wl.batch)
+    ref = oracle.conv2d(x.double().numpy(), pr.wbar, (1, 1), (1, 1))
+    assert rel_err(y.double().cpu().numpy(), ref) <= 1e-5
+
+
+def test_config1_full_size_sampled():
+    wl = workloads.config1()
+    y, pr, x = _run_layer(wl.layers[0], wl.batch)
+    _check_sampled(wl.layers[0], wl.batch, "f32", "f32", y, pr, x)
+
+
+@pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
+def test_config4_full_size_sampled(out_dtype):
+    wl = workloads.config4(out_dtype)
+    y, pr, x = _run_layer(wl.layers[0], wl.batch, "bf16", out_dtype)
+    _check_sampled(wl.layers[0], wl.batch, "bf16", out_dtype, y, pr, x, count=4000)
+
+
+_R50 = workloads.resnet50_convs()
+
+
+@pytest.mark.parametrize("li", range(len(_R50)), ids=[l.name for l in _R50])
+def test_config2_resnet50_layer_sampled(li):
+    layer = _R50[li]
+    print(f"resnet50 layer {layer.name}", flush=True)
+    y, pr, x = _run_layer(layer, 64)
+    _check_sampled(layer, 64, "f32", "f32", y, pr, x, count=1500, seed=li)
+
+
+_MB = workloads.mobilenet_v2_pointwise(4, 0.5)
+
+
+@pytest.mark.parametrize("li", range(len(_MB)), ids=[l.name for l in _MB])
+def test_config3_mobilenet_v2_layer_sampled(li):
+    """All twelve (N, p) sub-configurations on one layer's input (the input
+    depends only on the layer, not on N or p)."""
+    base = _MB[li]
+    print(f"mobilenet-v2 layer {base.name}", flush=True)
+    w, x = workloads.gen_layer(base, 128)
+    xd = x.cuda()
+    x64 = x.double().numpy()
+    for N in (4, 8, 16, 32):
+        for p in (0.3, 0.5, 0.7):
+            packed = onexn.prepare_layer(w, N, p, False)
+            y = packed.forward(xd)
+            torch.cuda.synchronize()
+            pr = oracle.prune(w.double().numpy(), N, p, False)
+            assert packed.t == pr.t
+            idx = sample_indices(tuple(y.shape), 600, li * 31 + N, N)
+            got = y.reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
+            ref = oracle.conv2d_at(x64, pr.wbar, idx)
+            assert rel_err(got, ref) <= 1e-5, (base.name, N, p)
