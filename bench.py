@@ -135,29 +135,55 @@ def main():
         del x, w
 
     stream = torch.cuda.current_stream(dev)
+    # One pre-marshalled launch per (layer, buffer copy); a step issues one per layer.
+    calls = []
+    for layer, packed, xs, ys in prepared:
+        calls.append([onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
+                                      layer.stride, layer.pad, "nchw", stream.cuda_stream)
+                      for r in range(len(xs))])
 
     def step(i):
-        for layer, packed, xs, ys in prepared:
-            r = i % len(xs)
-            packed.forward(xs[r], layer.stride, layer.pad, "nchw", odt, out=ys[r],
-                           stream=stream.cuda_stream)
+        for per_layer in calls:
+            per_layer[i % len(per_layer)]()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    # Timed region: K steps, events around every step on the launch stream.
+    # Host-side launch cost per step, to size the stall that keeps the GPU from
+    # draining the queue while the timed steps are being enqueued.
+    h0 = time.perf_counter()
+    for i in range(10):
+        step(i)
+    host_step_s = (time.perf_counter() - h0) / 10
+    torch.cuda.synchronize()
+    cyc0 = torch.cuda.Event(enable_timing=True)
+    cyc1 = torch.cuda.Event(enable_timing=True)
+    cyc0.record(stream)
+    torch.cuda._sleep(1_000_000)
+    cyc1.record(stream)
+    torch.cuda.synchronize()
+    cycles_per_ms = 1_000_000 / max(cyc0.elapsed_time(cyc1), 1e-3)
+    stall_ms = 2.0 * host_step_s * 1e3 * (args.steps + 2) + 5.0
+
+    # Timed region: the stream is held by a spin kernel while all K steps (and
+    # an event pair around each) are enqueued, so the GPU then runs them back
+    # to back and the events time the kernels, not the host.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     t_all0 = torch.cuda.Event(enable_timing=True)
     t_all1 = torch.cuda.Event(enable_timing=True)
+    stall_end = torch.cuda.Event()
     torch.cuda.synchronize()
+    torch.cuda._sleep(int(stall_ms * cycles_per_ms))
+    stall_end.record(stream)
     t_all0.record(stream)
     for i in range(args.steps):
         ev[i][0].record(stream)
         step(args.warmup + i)
         ev[i][1].record(stream)
     t_all1.record(stream)
+    host_ahead = not stall_end.query()     # the stall was still running: no gaps
     torch.cuda.synchronize()
     total_ms = t_all0.elapsed_time(t_all1)
     per_step = sorted(a.elapsed_time(b) for a, b in ev)
@@ -204,6 +230,8 @@ def main():
         "roofline": {"bound": bound, "achieved": round(achieved, 3), "peak": pk, "unit": unit,
                      "frac": round(achieved / pk, 4), "traffic": traffic},
         "host_prepare_s": round(t_host, 3),
+        "host_enqueued_ahead": host_ahead,
+        "host_launch_us_per_step": round(host_step_s * 1e6, 1),
     }
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline(wl.layers, batch, wl, args.cpu_budget)

@@ -168,12 +168,37 @@ def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: tor
         raise ValueError("out has the wrong shape, dtype or layout")
     if stream is None:
         stream = torch.cuda.current_stream(x.device).cuda_stream
-    st = load_library().onexn_conv2d_fwd(
-        P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype),
-        int(n), m, kh, kw, N, t, x.data_ptr(), _dtype_code(x.dtype), lay, B, H, W, stride[0],
-        stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt), stream)
-    _check(st, "onexn_conv2d_fwd")
+    args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype),
+            int(n), m, kh, kw, N, t, x.data_ptr(), _dtype_code(x.dtype), lay, B, H, W, stride[0],
+            stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt), stream)
+    _check(load_library().onexn_conv2d_fwd(*args), "onexn_conv2d_fwd")
     return out
+
+
+class BoundConv:
+    """A conv2d_fwd call with its arguments marshalled once; calling it
+    re-issues the same launch (same tensors, same stream).  The tensors must
+    stay alive and unmoved while this object is used."""
+
+    def __init__(self, P, I, D, n, x, out, stride=1, pad=0, layout="nchw", stream=None):
+        conv2d_fwd(P, I, D, n, x, stride, pad, layout, out.dtype, out, stream)   # validates
+        t, N, kh, kw = D.shape
+        lay = {"nchw": NCHW, "nhwc": NHWC}[layout]
+        B, m, H, W = x.shape if lay == NCHW else (x.shape[0], x.shape[3], x.shape[1], x.shape[2])
+        stride, pad = _pair(stride), _pair(pad)
+        if stream is None:
+            stream = torch.cuda.current_stream(x.device).cuda_stream
+        self._keep = (P, I, D, x, out)
+        self._fn = load_library().onexn_conv2d_fwd
+        self._args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0,
+                      _dtype_code(D.dtype), int(n), m, kh, kw, N, t, x.data_ptr(),
+                      _dtype_code(x.dtype), lay, B, H, W, stride[0], stride[1], pad[0], pad[1],
+                      out.data_ptr(), _dtype_code(out.dtype), stream)
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != ONEXN_OK:
+            _check(st, "onexn_conv2d_fwd")
 
 
 @dataclass
@@ -209,6 +234,6 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
     return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
 
 
-__all__ = ["BF16", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
+__all__ = ["BF16", "BoundConv", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
            "prepare_layer", "status_string"]

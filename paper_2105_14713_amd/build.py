@@ -19,6 +19,7 @@ ARCH = "gfx950"
 
 # Packed fp32 VALU ops are disabled for all device code (see the kernel notes).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+HIP_SOURCES = ["onexn_conv.hip", "conv_generic.hip", "conv_pointwise.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I" + INC, "-I" + CSRC]
 
 
@@ -31,12 +32,23 @@ def _run(cmd, verbose):
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT, exist_ok=True)
     host_o = os.path.join(OUT, "onexn_host.o")
-    conv_o = os.path.join(OUT, "onexn_conv.o")
-    _run(["g++"] + COMMON + ["-c", os.path.join(CSRC, "onexn_host.cpp"), "-o", host_o], verbose)
-    _run([HIPCC, "--offload-arch=" + ARCH] + COMMON + DEVICE_FLAGS +
-         ["-c", os.path.join(CSRC, "onexn_conv.hip"), "-o", conv_o], verbose)
+    jobs = [(["g++"] + COMMON + ["-c", os.path.join(CSRC, "onexn_host.cpp"), "-o", host_o])]
+    objs = [host_o]
+    for src in HIP_SOURCES:
+        obj = os.path.join(OUT, src.replace(".hip", ".o"))
+        jobs.append([HIPCC, "--offload-arch=" + ARCH] + COMMON + DEVICE_FLAGS +
+                    ["-c", os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
+    procs = []
+    for cmd in jobs:
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((cmd, subprocess.Popen(cmd)))
+    for cmd, proc in procs:
+        if proc.wait() != 0:
+            raise subprocess.CalledProcessError(proc.returncode, cmd)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", host_o, conv_o, "-o", tmp], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

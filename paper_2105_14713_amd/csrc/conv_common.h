@@ -1,0 +1,176 @@
+// Device-side definitions shared by the convolution kernels of libonexn.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <type_traits>
+
+#include "onexn_internal.h"
+
+namespace onexn {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;   // 4 waves of 64
+constexpr int kXcds = 8;        // MI355X dispatches workgroups round-robin over 8 XCDs
+
+struct ConvArgs {
+    const int32_t* P;
+    const int32_t* I;
+    const void* D;
+    const void* x;
+    void* y;
+    int32_t n, m, kh, kw, KK, N, G;
+    int32_t H, W, Ho, Wo, HWo;
+    int32_t sh, sw, ph, pw;
+    int32_t t;          // entries of I (kept blocks)
+    int32_t npix;       // batch * Ho * Wo
+    int64_t x_img;      // elements per input image
+    int32_t x_c, x_row, x_col;
+    int64_t y_img;      // elements per output image
+    int32_t y_c, y_pix;
+    int32_t total;      // workgroups in the grid
+    int32_t tpw;        // pixel tiles per workgroup (kernels that walk several)
+};
+
+// ---------------------------------------------------------------------------
+// Element helpers.  bf16 is carried as raw uint16_t bits.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { return f32_to_bf16(v); }
+
+// Physical workgroup id -> logical id such that each XCD gets a contiguous
+// range of logical ids (workgroup i runs on XCD i % 8).
+__device__ __forceinline__ int32_t xcd_remap(int32_t i, int32_t total) {
+    const int32_t x = i % kXcds, local = i / kXcds;
+    const int32_t q = total / kXcds, rmd = total % kXcds;
+    return x * q + min(x, rmd) + local;
+}
+
+// Kept-block range of col-group g, clamped to [0, t].
+__device__ __forceinline__ void group_range(const ConvArgs& a, int32_t g, int32_t& zb, int32_t& ze) {
+    zb = a.P[g];
+    ze = a.P[g + 1];
+    zb = max(0, min(zb, a.t));
+    ze = max(zb, min(ze, a.t));
+}
+
+// Per-lane view of one output pixel.  All offsets are element offsets.
+struct PixelPos {
+    int64_t xoff;    // x offset of (image, ih0, iw0); only dereferenced at in-bounds taps
+    int64_t ybase;   // y offset of the pixel at output channel 0
+    int32_t ih0, iw0;
+    bool valid;
+};
+
+__device__ __forceinline__ PixelPos pixel_pos(const ConvArgs& a, int32_t p) {
+    PixelPos r;
+    r.valid = p < a.npix;
+    if (!r.valid) p = 0;
+    const int32_t b = p / a.HWo;
+    const int32_t hw = p - b * a.HWo;
+    const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+    r.ih0 = oh * a.sh - a.ph;
+    r.iw0 = ow * a.sw - a.pw;
+    r.xoff = int64_t(b) * a.x_img + int64_t(r.ih0) * a.x_row + int64_t(r.iw0) * a.x_col;
+    r.ybase = int64_t(b) * a.y_img + int64_t(hw) * a.y_pix;
+    return r;
+}
+
+// Position along a col-group's contraction: kappa = zz*kh*kw + q*kw + r, i.e.
+// block zz (input channel I[zb + zz]) at kernel tap (q, r).  Every field is
+// wave-uniform, so the walk, the I[] lookups and the weight lookups stay on the
+// scalar unit and the gathered loads of a batch can all be in flight at once.
+struct KapWalk {
+    int32_t zz, q, r;
+};
+
+template <bool kUnit>
+__device__ __forceinline__ KapWalk walk_at(const ConvArgs& a, int32_t kap) {
+    if (kUnit) return {kap, 0, 0};
+    const int32_t zz = kap / a.KK, tap = kap - zz * a.KK;
+    const int32_t q = tap / a.kw, r = tap - q * a.kw;
+    return {__builtin_amdgcn_readfirstlane(zz), __builtin_amdgcn_readfirstlane(q),
+            __builtin_amdgcn_readfirstlane(r)};
+}
+
+template <bool kUnit>
+__device__ __forceinline__ void walk_step(const ConvArgs& a, KapWalk& w) {
+    if (kUnit) {
+        ++w.zz;
+        return;
+    }
+    if (++w.r == a.kw) {
+        w.r = 0;
+        if (++w.q == a.kh) {
+            w.q = 0;
+            ++w.zz;
+        }
+    }
+}
+
+// Input channel at walk position w, or -1 when kappa is past the end (ok ==
+// false) or I holds an out-of-range channel.  The I read is clamped to the
+// col-group's last entry, so it never leaves the array.
+__device__ __forceinline__ int32_t walk_channel(const ConvArgs& a, const KapWalk& w, int32_t zb,
+                                                int32_t ze, bool ok) {
+    const int32_t c = a.I[min(zb + w.zz, ze - 1)];
+    return (ok && c >= 0 && c < a.m) ? c : -1;
+}
+
+// One gathered input value: channel c (>= 0) at tap (w.q, w.r) under the pixel,
+// 0 in the zero padding and for invalid pixels.
+template <bool kUnit, typename TX>
+__device__ __forceinline__ TX gather_x(const ConvArgs& a, const TX* __restrict__ x,
+                                       const PixelPos& pp, int32_t c, const KapWalk& w) {
+    const int64_t uoff = int64_t(c) * a.x_c + int64_t(w.q) * a.x_row + int64_t(w.r) * a.x_col;
+    bool in = pp.valid;
+    if (!kUnit) {
+        const int32_t ih = pp.ih0 + w.q, iw = pp.iw0 + w.r;
+        in = in && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    }
+    return in ? x[pp.xoff + uoff] : TX(0);
+}
+
+
+// Compute units of the current device (queried once per device).
+int device_cu_count();
+
+// Kernel families (each defined in its own translation unit).
+onexn_status launch_generic(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
+bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_pointwise(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
+
+// Launches `kernel` on a 1-D grid of `total` workgroups.
+template <typename K>
+onexn_status launch_grid(K kernel, ConvArgs& a, int64_t total, hipStream_t stream,
+                         int threads = kThreads) {
+    if (total < 1 || total > INT32_MAX / threads)
+        return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: grid of %lld workgroups is out of range",
+                    (long long)total);
+    a.total = int32_t(total);
+    hipLaunchKernelGGL(kernel, dim3(uint32_t(total)), dim3(threads), 0, stream, a);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess)
+        return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(err));
+    return ONEXN_OK;
+}
+
+}  // namespace onexn

@@ -249,3 +249,21 @@ def test_config3_mobilenet_v2_layer_sampled(li):
             got = y.reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
             ref = oracle.conv2d_at(x64, pr.wbar, idx)
             assert rel_err(got, ref) <= 1e-5, (base.name, N, p)
+
+
+@pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
+@pytest.mark.parametrize("wpg", ["1", "2", "4", "8"])
+@pytest.mark.parametrize("N", [16, 32])
+def test_pointwise_variants_integer_exact(N, wpg, hw, monkeypatch):
+    """Every waves-per-col-group variant of the pointwise kernel: several
+    channel chunks with a ragged last one (m = 300 > the largest chunk), col-group
+    sets with a partial last set and a ragged last col-group, and p from dense
+    to nearly empty (col-groups with no entries in some chunks)."""
+    monkeypatch.setenv("ONEXN_PW_WPG", wpg)
+    n = 9 * N + N // 2
+    w, x = workloads.gen_integer_layer(seed=N, cout=n, cin=300, k=1, batch=2, H=hw[0], W=hw[1],
+                                       wmax=1, xmax=2)
+    for p in (0.0, 0.5, 0.95):
+        y, _ = gpu_conv(w, x, N, p, True, 1, 0)
+        ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
+        np.testing.assert_array_equal(y, ref)
