@@ -130,6 +130,8 @@ def test_batch_zero_is_noop():
     dict(n=33, m=600, k=3, N=32, B=1, H=6, s=1, pd=1),   # long contraction, 1-row last group
     dict(n=100, m=17, k=1, N=4, B=5, H=13, s=1, pd=0),   # many groups, ragged pixel tail
     dict(n=48, m=7, k=5, N=16, B=2, H=9, s=3, pd=2),     # 5x5, stride 3
+    dict(n=8, m=3, k=16, N=8, B=1, H=20, s=8, pd=15),    # largest kernel, stride and pad
+    dict(n=20, m=2, k=16, N=16, B=2, H=17, s=8, pd=15),  # the same on the MFMA kernel
 ])
 def test_edge_shapes_integer_exact(case):
     c = case
