@@ -105,8 +105,10 @@ onexn_status onexn_pack(const void* w, onexn_dtype wdt, int32_t n, int32_t m, in
  * Accumulation is fp32.
  *
  * P_dev, I_dev, D_dev: device BSR arrays from onexn_pack (G+1, t, t*N*kh*kw
- *         entries).  Entries of I outside [0, m) are skipped and P is clamped
- *         to [0, t], so malformed arrays cannot cause out-of-bounds reads.
+ *         entries).  P is clamped to [0, t] and entries of I outside [0, m)
+ *         contribute nothing, so malformed arrays cannot cause out-of-bounds
+ *         reads.  With I not ascending within a col-group the result is
+ *         unspecified (still no out-of-bounds access).
  * x_dev:  device input [batch][m][H][W] (NCHW) or [batch][H][W][m] (NHWC).
  * y_dev:  device output [batch][n][Ho][Wo] or [batch][Ho][Wo][n] (same layout
  *         as x), Ho = (H + 2*pad_h - kh)/stride_h + 1, likewise Wo.  Every

@@ -34,7 +34,9 @@ struct ConvArgs {
     int64_t y_img;      // elements per output image
     int32_t y_c, y_pix;
     int32_t total;      // workgroups in the grid
-    int32_t tpw;        // pixel tiles per workgroup (kernels that walk several)
+    int32_t tile_ranges;   // streamed pointwise kernel: pixel-tile ranges per col-group set
+    int32_t slices;        // resident-tile pointwise kernel: slices per pixel tile,
+    int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder)
 };
 
 // ---------------------------------------------------------------------------
@@ -157,6 +159,8 @@ int device_cu_count();
 onexn_status launch_generic(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
 bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 onexn_status launch_pointwise(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
+bool pw_tile_applies(const ConvArgs& a);
+onexn_status launch_pw_tile(ConvArgs a, hipStream_t stream);
 
 // Launches `kernel` on a 1-D grid of `total` workgroups.
 template <typename K>

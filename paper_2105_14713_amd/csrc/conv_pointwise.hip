@@ -7,19 +7,28 @@
 // blocks select rows of the input matrix X[channel][pixel], and the N weights
 // of a block are one contiguous row of D.
 //
-// Work split.  A workgroup of 8 waves owns a tile of PT = 64*WPG pixels and
-// 8/WPG consecutive col-groups; each col-group is computed by WPG waves, one
-// 64-pixel slice each.  Input channels are walked in chunks of KC: a chunk of
-// X (KC rows x PT pixels) is read once from global memory (coalesced, one
-// chunk ahead) into LDS and shared by all col-groups of the workgroup, so X
-// crosses L2 -> CU only G*WPG/8 times.
+// Work split.  A workgroup has 8 compute waves and one loader wave.  It owns
+// 8/WPG consecutive col-groups (each computed by WPG compute waves, one
+// 64-pixel slice each) and a contiguous range of pixel tiles of PT = 64*WPG
+// pixels, which it walks in order.  Input channels are walked in chunks of
+// KC: the X stream of the workgroup is the sequence (tile, chunk), and chunk
+// c of a tile (KC rows x PT pixels, 16 KB) is copied once from global memory
+// straight into LDS by the loader wave (global_load_lds, 16 bytes per lane
+// where rows allow it) into a ring of kPwRing buffers, several chunks ahead
+// of use, and shared by all col-groups of the workgroup.  The loader is a
+// wave of its own because a wave's vector loads complete in issue order: a
+// compute wave that also streamed X would wait for X behind every weight
+// load.  A workgroup barrier per chunk hands a landed chunk to the compute
+// waves and frees the buffer of the chunk before it.
 //
-// Each wave streams its own col-group's BSR entries: the entries of a chunk
-// are a contiguous run (I is ascending; the run bounds are computed once per
-// wave), taken in blocks of 8 MFMA steps.  For a block the wave reads the I
-// values (one coalesced load, rows handed to lane groups with ds_bpermute) and
-// the weights (one coalesced load per step) straight from global memory, one
-// block ahead of use, so the inner loop is 8 LDS reads of X and 8*NB MFMAs.
+// Each compute wave streams its own col-group's BSR entries: the entries of
+// a chunk are a contiguous run (I is ascending; the run bounds are computed
+// once per wave), taken in blocks of 8 MFMA steps.  For a block the wave
+// reads the I values (one coalesced load, rows handed to lane groups with
+// ds_bpermute) and the weights (one coalesced load per step) straight from
+// global memory, one block ahead of use, so the inner loop is 8 LDS reads of
+// X and 8*NB MFMAs.  Entries whose channel lies outside [0, m) read a row of
+// zeros.
 //
 //   N = 16: v_mfma_f32_16x16x4f32, 4 kept blocks per step (lane group l/16),
 //           NB = 4 column blocks per wave: MFMA column n of block e is pixel
@@ -27,44 +36,24 @@
 //   N = 32: v_mfma_f32_32x32x2f32, 2 kept blocks per step, NB = 2.
 #include <cstdio>
 #include <cstdlib>
+#include <string>
 
-#include "conv_common.h"
+#include "pw_common.h"
 
 namespace onexn {
 namespace {
 
-constexpr int kPwThreads = 512;   // 8 waves
-constexpr int kPwWaves = kPwThreads / 64;
+constexpr int kPwWaves = 8;                        // compute waves
+constexpr int kPwThreads = 64 * (kPwWaves + 1);    // + the loader wave
 constexpr int kPwWavePx = 64;     // pixels per wave
 constexpr int kPwLdsFloats = 4096;   // one X chunk buffer: 16 KB
+constexpr int kPwRing = 6;        // X chunk buffers
 constexpr int kPwSteps = 8;       // MFMA steps per block
 constexpr int kPwMaxChunks = 64;  // channel chunks a layer may have
 
-template <int N> struct PwMfma;
-template <> struct PwMfma<16> {   // 16x16x4 f32
-    typedef f32x4 acc_t;
-    static constexpr int KS = 4, ACC = 4;
-    __device__ static acc_t step(float a, float b, acc_t c) {
-        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-    }
-    __device__ static int row(int lane, int r) { return 4 * (lane / 16) + r; }
-};
-template <> struct PwMfma<32> {   // 32x32x2 f32
-    typedef f32x16 acc_t;
-    static constexpr int KS = 2, ACC = 16;
-    __device__ static acc_t step(float a, float b, acc_t c) {
-        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-    }
-    __device__ static int row(int lane, int r) { return 8 * (r / 4) + 4 * (lane / 32) + (r % 4); }
-};
-
-template <int NB> struct VecF;
-template <> struct VecF<2> { typedef float T __attribute__((ext_vector_type(2))); };
-template <> struct VecF<4> { typedef f32x4 T; };
-
 template <int N, int WPG>
 struct PwShape {
-    static constexpr int PT = kPwWavePx * WPG;            // pixels per workgroup
+    static constexpr int PT = kPwWavePx * WPG;            // pixels per tile
     static constexpr int S = kPwWaves / WPG;              // col-groups per workgroup
     static constexpr int KC = kPwLdsFloats / PT;          // channels per chunk
     static constexpr int NB = kPwWavePx / N;              // MFMA column blocks per wave
@@ -72,20 +61,24 @@ struct PwShape {
 };
 
 template <int N, int WPG, bool kVec4>
-__global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu(4))) pw_mfma_f32(ConvArgs a) {
+__global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef PwShape<N, WPG> SH;
     typedef typename M::acc_t acc_t;
     constexpr int PT = SH::PT, S = SH::S, KC = SH::KC, NB = SH::NB, BLK = SH::BLK;
     constexpr int KS = M::KS, STEPS = kPwSteps;
-    constexpr int QPR = PT / 4;                 // pixel quads per X row
-    constexpr int RG = kPwThreads / QPR;        // X rows loaded in parallel
-    constexpr int XJ = KC / RG;                 // quads per thread per chunk
+    // Loads into LDS per chunk (loader wave): 16 bytes per lane when pixel
+    // quads are aligned and never straddle an image, else 4 bytes per lane.
+    constexpr int EB = kVec4 ? 4 : 1;                 // floats per lane per load
+    constexpr int ND = kPwLdsFloats / (EB * 64);      // loads per chunk
+    constexpr int QPR = PT / EB;                      // lane slots per X row
+    constexpr int ROWB = PT * 4;                      // bytes per X row in LDS
+    constexpr int ZERO_OFF = kPwRing * kPwLdsFloats * 4;  // byte offset of the zero row
     static_assert(64 / N == KS && BLK <= 64, "lane groups carry a step's kept blocks");
-    static_assert(XJ >= 1 && KC % RG == 0, "tile shape");
+    static_assert(KC * PT == kPwLdsFloats && KC >= 1, "tile shape");
     typedef typename VecF<NB>::T vec_t;
 
-    __shared__ __attribute__((aligned(16))) float sX[2][KC * PT];
+    __shared__ __attribute__((aligned(16))) float sX[kPwRing * kPwLdsFloats + PT];
     __shared__ int32_t sBnd[kPwWaves][kPwMaxChunks + 1];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -93,15 +86,69 @@ __global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu
     const int32_t GS = (a.G + S - 1) / S;
     const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
     const int32_t gs = L % GS;
-    // This workgroup walks pixel tiles [tile0, tile0 + nt) for col-group set gs.
-    const int32_t tile0 = (L / GS) * a.tpw;
-    const int32_t nt = min(a.tpw, (a.npix + PT - 1) / PT - tile0);
+    // This workgroup walks pixel tiles [tile0, tile0 + nt) for col-group set
+    // gs: range L / GS of a.tile_ranges near-equal ranges.
+    const int32_t tiles = (a.npix + PT - 1) / PT;
+    const int32_t rg = L / GS;
+    const int32_t tile0 = int32_t(int64_t(rg) * tiles / a.tile_ranges);
+    const int32_t nt = int32_t(int64_t(rg + 1) * tiles / a.tile_ranges) - tile0;
+    const int32_t nch = (a.m + KC - 1) / KC;
+    const int32_t nel = nt * nch;   // X stream: element e = chunk e % nch of tile tile0 + e / nch
+
+    if (wave == kPwWaves) {
+        // Loader wave.  Element e goes to ring buffer e % kPwRing.  Load j
+        // covers LDS floats [j*64*EB, (j+1)*64*EB) of the buffer
+        // (lane-contiguous, as loads into LDS require): lane slot f = j*64 +
+        // lane is row f / QPR, pixel EB*(f % QPR) of the tile.  Rows past m
+        // and pixels past the last image read a valid element instead (never
+        // used: rows past m are never selected, pixels past the end are
+        // never stored).
+        const float* __restrict__ x = static_cast<const float*>(a.x);
+        auto issue_x = [&](int32_t e) {
+            const int32_t tile = tile0 + e / nch, c = e % nch;
+            float* dst = sX + (e % kPwRing) * kPwLdsFloats;
+#pragma unroll 4
+            for (int j = 0; j < ND; ++j) {
+                const int32_t f = j * 64 + lane;
+                int32_t p = tile * PT + EB * (f % QPR);
+                p = p < a.npix ? p : 0;
+                const int32_t b = p / a.HWo;
+                const int32_t ch = min(c * KC + f / QPR, a.m - 1);
+                const float* src = x + int64_t(b) * a.x_img + int64_t(ch) * a.x_c + (p - b * a.HWo);
+                if constexpr (kVec4)
+                    __builtin_amdgcn_global_load_lds(src, dst + j * 64 * EB, 16, 0, 0);
+                else
+                    __builtin_amdgcn_global_load_lds(src, dst + j * 64 * EB, 4, 0, 0);
+            }
+        };
+        // Waits for element e's loads, `newer` elements having been issued
+        // after it.  Loads complete in issue order, so at most newer*ND
+        // outstanding loads means e has landed (the count saturates at the
+        // counter's range, which only waits longer).
+        auto wait_x = [&](int32_t newer) {
+            const int32_t k = newer * ND;
+            if (k >= 63) wait_vmem<63>();
+            else if (k >= 48) wait_vmem<48>();
+            else if (k >= 32) wait_vmem<32>();
+            else if (k >= 16) wait_vmem<16>();
+            else wait_vmem<0>();
+        };
+        static_assert(ND % 16 == 0, "wait_x counts in steps of 16 loads");
+        for (int32_t e = 0; e < min(kPwRing - 1, nel); ++e) issue_x(e);
+        for (int i = lane; i < PT; i += 64) sX[kPwRing * kPwLdsFloats + i] = 0.f;
+        wait_lgkm();
+        __builtin_amdgcn_s_barrier();   // set-up done
+        for (int32_t el = 0; el < nel; ++el) {
+            wait_x(min(el + kPwRing - 2, nel - 1) - el);
+            __builtin_amdgcn_s_barrier();   // element el visible; buffer of el - 1 free
+            if (el + kPwRing - 1 < nel) issue_x(el + kPwRing - 1);
+        }
+        return;
+    }
+
     const int32_t g = gs * S + wave / WPG;      // this wave's col-group
     const int slice = wave % WPG;               // this wave's 64-pixel slice
-    const float* __restrict__ x = static_cast<const float*>(a.x);
     const float* __restrict__ D = static_cast<const float*>(a.D);
-    const int32_t nch = (a.m + KC - 1) / KC;
-
     int32_t zb = 0, ze = 0;
     if (g < a.G) group_range(a, g, zb, ze);
 
@@ -118,64 +165,24 @@ __global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu
         }
     }
 
-    // X loader role: pixel quad qd of a tile, rows rg, rg + RG, ...  Element e
-    // of the X stream is chunk e % nch of tile tile0 + e / nch.
-    const int qd = tid % QPR, rg = tid / QPR;
-    f32x4 xr[XJ];
-    auto fetch_x = [&](int32_t e) {
-        const int32_t tile = tile0 + e / nch, c = e % nch;
-        int64_t xo[4];
-        bool xv[4];
-#pragma unroll
-        for (int q = 0; q < (kVec4 ? 1 : 4); ++q) {
-            const int32_t p = tile * PT + 4 * qd + q;
-            xv[q] = p < a.npix;
-            const int32_t pp = xv[q] ? p : 0;
-            const int32_t b = pp / a.HWo;
-            xo[q] = int64_t(b) * a.x_img + (pp - b * a.HWo);
-        }
-#pragma unroll
-        for (int j = 0; j < XJ; ++j) {
-            const int32_t ch = c * KC + rg + j * RG;
-            const bool chok = ch < a.m;
-            const int64_t co = int64_t(ch) * a.x_c;
-            if (kVec4) {
-                f32x4 v = {0.f, 0.f, 0.f, 0.f};
-                if (chok && xv[0]) v = *reinterpret_cast<const f32x4*>(x + xo[0] + co);
-                xr[j] = v;
-            } else {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) xr[j][q] = (chok && xv[q]) ? x[xo[q] + co] : 0.f;
-            }
-        }
-    };
-    auto stash_x = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < XJ; ++j)
-            *reinterpret_cast<f32x4*>(&sX[buf][(rg + j * RG) * PT + 4 * qd]) = xr[j];
-    };
-
     // One block of the wave's BSR entries: [s, s + len), len <= BLK, all in
-    // one channel chunk with base channel c0.
+    // one chunk.  The loads are only issued here; nothing consumes them until
+    // the block is run (one block later), so they stay in flight across the
+    // MFMAs of the block before.  Indices past len are clamped to the block's
+    // last entry: its weights are loaded again, and the entry reads the zero
+    // row of X.
     struct Block {
-        int32_t off;         // lane i < len: LDS byte offset of entry i's X row, else 0
+        int32_t ch;          // lane i: input channel of entry min(i, len - 1)
         float av[STEPS];     // weight of step ks for this lane's (lane group, output)
     };
     const int lg = lane / N, lo = lane % N;
-    auto load_block = [&](Block& bk, int32_t s, int32_t len, int32_t c0) {
+    auto load_block = [&](Block& bk, int32_t s, int32_t len) {
         if (len <= 0) return;   // uniform: nothing left for this wave
-        // Clamped indices keep every load inside the block; the selects zero
-        // the entries past len (weight 0, X row 0).
         const int32_t* Ib = a.I + s;
         const float* Db = D + int64_t(s) * N;
-        const int32_t ch = Ib[min(lane, len - 1)];
-        bk.off = lane < len ? min(max(ch - c0, 0), KC - 1) * (PT * 4) : 0;
+        bk.ch = Ib[min(lane, len - 1)];
 #pragma unroll
-        for (int ks = 0; ks < STEPS; ++ks) {
-            const int i = ks * KS + lg;
-            const float v = Db[uint32_t(min(i, len - 1) * N + lo)];
-            bk.av[ks] = i < len ? v : 0.f;
-        }
+        for (int ks = 0; ks < STEPS; ++ks) bk.av[ks] = Db[uint32_t(min(ks * KS + lg, len - 1) * N + lo)];
     };
 
     acc_t acc[NB];
@@ -184,14 +191,19 @@ __global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) acc[e][r] = 0.f;
 
-    // Multiplies one loaded block against X chunk buffer `buf`.
-    auto run_block = [&](const Block& bk, int32_t len, int buf) {
-        const char* xs = reinterpret_cast<const char*>(&sX[buf][slice * kPwWavePx + NB * lo]);
+    // Multiplies one loaded block against the X rows it names: the block's
+    // chunk has base channel c0 and sits in ring buffer buf.  Lanes i >= len
+    // and channels outside the chunk or [0, m) read the zero row.
+    const char* xs = reinterpret_cast<const char*>(sX + slice * kPwWavePx + NB * lo);
+    auto run_block = [&](const Block& bk, int32_t len, int32_t c0, int32_t buf) {
+        const int32_t rel = bk.ch - c0;
+        const bool ok = lane < len && rel >= 0 && rel < KC && bk.ch < a.m;
+        const int32_t off = ok ? (buf * KC + rel) * ROWB : ZERO_OFF;
         vec_t bv[STEPS];
 #pragma unroll
         for (int ks = 0; ks < STEPS; ++ks) {
-            const int32_t off = __builtin_amdgcn_ds_bpermute(4 * (ks * KS + lg), bk.off);
-            bv[ks] = *reinterpret_cast<const vec_t*>(xs + off);
+            const int32_t o = __builtin_amdgcn_ds_bpermute(4 * (ks * KS + lg), off);
+            bv[ks] = *reinterpret_cast<const vec_t*>(xs + o);
         }
         // Keep all X reads of the block ahead of the (guarded) MFMAs.
 #pragma unroll
@@ -259,7 +271,8 @@ __global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu
     // same for every tile (it depends on the col-group only) and restarts at
     // each tile.  While a block is multiplied, the next one's loads are in
     // flight, including the first block of the next tile.
-    __syncthreads();   // run bounds visible
+    wait_lgkm();   // the run bounds are LDS stores
+    __builtin_amdgcn_s_barrier();
     struct Pos {
         int32_t t, c, s, e, len;   // tile, chunk, first entry, end of the chunk's run, entries
     };
@@ -285,31 +298,32 @@ __global__ void __launch_bounds__(kPwThreads) __attribute__((amdgpu_waves_per_eu
         if (r.len == 0 && q.t + 1 < nt) r = first(q.t + 1);
         return r;
     };
+    auto buf_of = [&](const Pos& q) { return (q.t * nch + q.c) % kPwRing; };
     Pos q0 = first(0);
     Block bk0, bk1;
-    load_block(bk0, q0.s, q0.len, q0.c * KC);
+    // The first block goes through bk1 like every later one, so that bk0's
+    // registers are only written by the copy in the loop and the waits for
+    // in-flight loads stay exact.
+    load_block(bk1, q0.s, q0.len);
+    asm volatile("" : "+v"(bk1.ch));
+#pragma unroll
+    for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(bk1.av[ks]));
+    bk0 = bk1;
 
-    fetch_x(0);
-    stash_x(0);
-    __syncthreads();
-    const int32_t nel = nt * nch;
     for (int32_t el = 0; el < nel; ++el) {
-        const int32_t tt = el / nch, c = el % nch;
-        if (el + 1 < nel) fetch_x(el + 1);
-        const int buf = el & 1;
+        const int32_t tt = el / nch, c = el - tt * nch;
+        __builtin_amdgcn_s_barrier();   // element el has landed in LDS
         while (q0.t == tt && q0.c == c && q0.len > 0) {
             const Pos q1 = after(q0);
-            load_block(bk1, q1.s, q1.len, q1.c * KC);
-            run_block(bk0, q0.len, buf);
+            load_block(bk1, q1.s, q1.len);
+            run_block(bk0, q0.len, q0.c * KC, buf_of(q0));
             // The next block's loads stay in flight across this block's MFMAs.
-            asm volatile("" : "+v"(bk1.off));
+            asm volatile("" : "+v"(bk1.ch));
 #pragma unroll
             for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(bk1.av[ks]));
             bk0 = bk1;
             q0 = q1;
         }
-        if (el + 1 < nel) stash_x((el + 1) & 1);
-        __syncthreads();
         if (c == nch - 1) epilogue(tile0 + tt);
     }
 }
@@ -328,15 +342,16 @@ int choose_wpg(const ConvArgs& a) {
     return 8;
 }
 
-// Pixel tiles per workgroup: one by default (measured fastest on the 28x28
-// layers: a workgroup that walks several tiles serialises their X fetches);
-// ONEXN_PW_TPW overrides it for A/B measurements.
-int32_t choose_tpw() {
-    if (const char* env = std::getenv("ONEXN_PW_TPW")) {
-        const int v = std::atoi(env);
-        if (v >= 1 && v <= 1024) return v;
+// Tile ranges per col-group set: one workgroup per compute unit in total
+// (one fits per CU), each walking its range so that its X stream never
+// drains; ONEXN_PW_RANGES overrides the count for A/B measurements.
+int64_t choose_ranges(int64_t tiles, int64_t gsets) {
+    if (const char* env = std::getenv("ONEXN_PW_RANGES")) {
+        const long v = std::atol(env);
+        if (v >= 1) return std::min<int64_t>(v, tiles);
     }
-    return 1;
+    const int64_t per_set = std::max<int64_t>(1, int64_t(device_cu_count()) / gsets);
+    return std::min<int64_t>(per_set, tiles);
 }
 
 template <int N, int WPG>
@@ -344,12 +359,12 @@ onexn_status launch_pw(ConvArgs a, hipStream_t s) {
     typedef PwShape<N, WPG> SH;
     const int64_t tiles = (int64_t(a.npix) + SH::PT - 1) / SH::PT;
     const int64_t gsets = (a.G + SH::S - 1) / SH::S;
-    a.tpw = choose_tpw();
-    const int64_t total = ((tiles + a.tpw - 1) / a.tpw) * gsets;
+    const int64_t ranges = choose_ranges(tiles, gsets);
+    a.tile_ranges = int32_t(ranges);
     const bool vec4 = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
                       (reinterpret_cast<uintptr_t>(a.y) & 15) == 0;
-    if (vec4) return launch_grid(pw_mfma_f32<N, WPG, true>, a, total, s, kPwThreads);
-    return launch_grid(pw_mfma_f32<N, WPG, false>, a, total, s, kPwThreads);
+    if (vec4) return launch_grid(pw_mfma_f32<N, WPG, true>, a, ranges * gsets, s, kPwThreads);
+    return launch_grid(pw_mfma_f32<N, WPG, false>, a, ranges * gsets, s, kPwThreads);
 }
 
 template <int N>
@@ -374,7 +389,15 @@ bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onex
     return a.m <= int64_t(kPwMaxChunks) * kc;
 }
 
+// The resident-tile kernel where the layer fits it, else the streamed one.
+// ONEXN_PW_KERNEL=stream or =tile forces one of them (for tests and A/B
+// measurements; =tile on a layer it does not fit is an error).
 onexn_status launch_pointwise(ConvArgs a, onexn_dtype, onexn_dtype, hipStream_t s) {
+    const char* env = std::getenv("ONEXN_PW_KERNEL");
+    const std::string force = env ? env : "";
+    if (force == "tile" && !pw_tile_applies(a))
+        return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: the resident-tile kernel does not fit this layer");
+    if (force != "stream" && pw_tile_applies(a)) return launch_pw_tile(a, s);
     return a.N == 16 ? launch_pw_n<16>(a, s) : launch_pw_n<32>(a, s);
 }
 

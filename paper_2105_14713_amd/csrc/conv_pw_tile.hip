@@ -1,0 +1,459 @@
+// Pointwise (1x1, stride 1, no padding, NCHW) 1xN-pruned convolution, fp32,
+// N in {16, 32}, for layers whose input-channel count lets a whole pixel tile
+// of X stay in LDS (m * 16..64 pixels * 4 bytes <= 64 KB).
+//
+// Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
+// (arXiv 2105.14713), Sec. 3.4, Eq. 8.  For a 1x1 kernel col-group g is the
+// contraction Y_g[N][pixels] = D_g^T[N][kept_g] * X[I_g][pixels]: its kept
+// blocks select rows of the input matrix X[channel][pixel], and the N weights
+// of a block are one contiguous row of D.
+//
+// Work split.  A pixel tile is SL slices of SW pixels; a unit of work is one
+// (slice, col-group) pair of a tile, and costs kept_g + 1 (the kept blocks,
+// plus its stores).  The (tile, unit) sequence, tile-major, is cut into one
+// contiguous range of equal cost per workgroup (one workgroup per CU), so
+// workgroups finish together however unevenly the col-groups are pruned
+// (output-channel rearrangement makes the first col-groups the heaviest).
+//
+// A workgroup has 15 compute waves and one loader wave, and two LDS buffers
+// that each hold all m rows of one tile's X.  The loader copies the tiles of
+// the range into the buffers in turn (global_load_lds, 16 bytes per lane
+// where pixel quads allow it): a tile is copied while the one before it is
+// computed.  It is a wave of its own because a wave's vector loads complete
+// in issue order: a compute wave that also copied X would wait for the copy
+// behind its next weight load.  Compute waves take the units of the landed
+// tile from an LDS counter until none is left and go straight on to the next
+// tile, so no wave waits for the others at tile ends.  LDS flags order the
+// two sides: `landed` (the loader has a tile in a buffer, counter reset) and
+// `done` (compute waves finished with a buffer's tile, so it may be reused).
+//
+// A wave computes a unit as a dense contraction over the col-group's kept
+// blocks, taken in blocks of 8 MFMA steps: for each block it reads the I
+// values (one coalesced load, rows handed to lane groups with ds_bpermute) and
+// the weights (one coalesced load per step) from global memory, one block
+// ahead of use, then 8 LDS reads of X and 8*NB MFMAs.  Entries whose channel
+// lies outside [0, m) read a row of zeros.
+//
+//   N = 16: v_mfma_f32_16x16x4f32, 4 kept blocks per step (lane group l/16).
+//   N = 32: v_mfma_f32_32x32x2f32, 2 kept blocks per step.
+//   NB = SW / (MFMA columns) column blocks per unit: MFMA column n of block e
+//   is pixel NB*n + e of the slice, so a lane reads NB consecutive pixels.
+#include <cstdlib>
+
+#include "pw_common.h"
+
+namespace onexn {
+namespace {
+
+constexpr int kTileCompute = 15;                        // compute waves
+constexpr int kTileThreads = 64 * (kTileCompute + 1);   // + the loader wave
+constexpr int kTileBufFloats = 16384;                   // one X tile buffer: 64 KB
+constexpr int kTileSteps = 8;                           // MFMA steps per block
+constexpr int kTileMaxG = 256;                          // col-groups a layer may have
+constexpr int32_t kBufferFlags = 0x00020000;            // buffer resource word 3: 32-bit raw data
+
+__device__ __forceinline__ int32_t lds_load(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_store(int32_t* p, int32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+template <int N, int SW, bool kVec4>
+__global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
+    typedef PwMfma<N> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int KS = M::KS, STEPS = kTileSteps, BLK = STEPS * KS;
+    constexpr int NB = SW / M::COLS;
+    constexpr int EB = kVec4 ? 4 : 1;   // floats per lane per X load
+    constexpr int ZERO_OFF = 2 * kTileBufFloats * 4;
+    static_assert(NB >= 1 && NB * M::COLS == SW, "slice width");
+    static_assert(64 / N == KS && BLK <= 64, "lane groups carry a step's kept blocks");
+    typedef typename VecF<NB>::T vec_t;
+
+    __shared__ __attribute__((aligned(16))) float sX[2 * kTileBufFloats + SW];
+    __shared__ int32_t sP[kTileMaxG + 1];   // P[g] + g: cost of the units before group g
+    __shared__ int32_t sNext[2], sLanded[2], sDone[2];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t G = a.G, SL = a.slices, PT = SL * SW;
+    const int32_t units = SL * G;
+    const int32_t slice_cost = a.t + G;
+    const int32_t tile_cost = slice_cost * SL;
+    const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
+    const int32_t W = a.total;
+    // Cost range [c0, c1) of this workgroup; the host split the total cost
+    // (below 2^31) into cost_q * W + cost_r.
+    const int32_t c0 = a.cost_q * L + a.cost_r * L / W;
+    const int32_t c1 = a.cost_q * (L + 1) + a.cost_r * (L + 1) / W;
+    if (c0 >= c1) return;   // the whole workgroup: nothing to do
+
+    // X copy of tile T into buffer b (loader wave).  The tile is m rows of
+    // spr = PT/EB lane slots (a power of two); lane slot f = j*64 + lane of
+    // load j is row f / spr, pixel EB*(f % spr), at LDS float offset f*EB, so
+    // each load's 64 slots are contiguous, as loads into LDS require.
+    //   spr <= 64: load j covers rows j*(64/spr) + lane/spr, and a lane keeps
+    //              one pixel for the whole tile.
+    //   spr > 64:  load j covers pixel block pb = j % nb (nb = spr/64) of row
+    //              j / nb, so a lane keeps one pixel per block.
+    // Each lane computes its pixel's address once per block and steps rows by
+    // pointer increments.  Pixels past the last image read a valid element
+    // instead (never stored).
+    const float* __restrict__ x = static_cast<const float*>(a.x);
+    const int32_t spr = PT / EB;
+    const int spr_shift = __builtin_ctz(uint32_t(spr));
+    auto pixel_src = [&](int32_t T, int32_t slot) {
+        int32_t p = T * PT + EB * slot;
+        p = p < a.npix ? p : 0;
+        const int32_t bi = p / a.HWo;
+        return x + int64_t(bi) * a.x_img + (p - bi * a.HWo);
+    };
+    auto dma = [&](const float* src, float* dst) {
+        if constexpr (kVec4)
+            __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+        else
+            __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
+    };
+    auto copy_tile = [&](int32_t T, int b) {
+        float* dst0 = sX + b * kTileBufFloats;
+        if (spr <= 64) {
+            const int32_t rpl = 64 >> spr_shift;           // rows per load
+            const int32_t row0 = lane >> spr_shift;
+            const float* src = pixel_src(T, lane & (spr - 1)) + int64_t(row0) * a.x_c;
+            const int64_t step = int64_t(rpl) * a.x_c;
+            for (int32_t j = 0; j * rpl < a.m; ++j, src += step)
+                if (j * rpl + row0 < a.m) dma(src, dst0 + j * 64 * EB);
+        } else {
+            const int32_t nb = spr >> 6;
+            for (int32_t pb = 0; pb < nb; ++pb) {
+                const float* src = pixel_src(T, 64 * pb + lane);
+                for (int32_t r = 0; r < a.m; ++r, src += a.x_c) dma(src, dst0 + (r * nb + pb) * 64 * EB);
+            }
+        }
+    };
+
+    const bool loader = wave == kTileCompute;
+    const int32_t Tfirst = c0 / tile_cost;
+    if (loader) copy_tile(Tfirst, 0);   // started before anything else
+    for (int i = tid; i <= G; i += kTileThreads) sP[i] = max(0, min(a.P[i], a.t)) + i;
+    for (int i = tid; i < SW; i += kTileThreads) sX[2 * kTileBufFloats + i] = 0.f;
+    if (tid < 2) {
+        sLanded[tid] = 0;
+        sDone[tid] = 0;
+    }
+    wait_lgkm();
+    __builtin_amdgcn_s_barrier();   // sP and the flags are set
+
+    // First unit at or after cost offset c: the tile's units sorted by
+    // start cost s*(t + G) + P[g] + g.
+    auto locate = [&](int32_t c, int32_t& tile, int32_t& unit) {
+        tile = c / tile_cost;
+        const int32_t r = c - tile * tile_cost;
+        const int32_t s = r / slice_cost;
+        const int32_t rr = r - s * slice_cost;
+        int32_t lo = 0, hi = G;   // first g in [0, G] with sP[g] >= rr
+        while (lo < hi) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (sP[mid] >= rr) hi = mid;
+            else lo = mid + 1;
+        }
+        unit = lo == G ? (s + 1) * G : s * G + lo;
+        if (unit >= units) {
+            ++tile;
+            unit = 0;
+        }
+    };
+    int32_t T0, u0, T1, u1;
+    locate(c0, T0, u0);
+    locate(c1, T1, u1);
+    T0 = __builtin_amdgcn_readfirstlane(T0);
+    u0 = __builtin_amdgcn_readfirstlane(u0);
+    T1 = __builtin_amdgcn_readfirstlane(T1);
+    u1 = __builtin_amdgcn_readfirstlane(u1);
+    // The workgroup's tiles are T0 .. Tlast; tile k of them (T0 + k) sits in
+    // buffer k % 2.  Its units are [ub, ue).
+    const int32_t ntiles = (u1 > 0 ? T1 + 1 : T1) - T0;
+    auto unit_begin = [&](int32_t k) { return k == 0 ? u0 : 0; };
+    auto unit_end = [&](int32_t k) { return T0 + k == T1 ? u1 : units; };
+
+    if (loader) {
+        for (int32_t k = 0; k < ntiles; ++k) {
+            const int b = k & 1;
+            if (k >= 2) {
+                // Buffer b is free once every compute wave is done with tile k - 2.
+                while (__builtin_amdgcn_readfirstlane(lds_load(&sDone[b])) < kTileCompute * (k / 2))
+                    __builtin_amdgcn_s_sleep(2);
+            }
+            if (k > 0 || Tfirst != T0) copy_tile(T0 + k, b);
+            if (lane == 0) lds_store(&sNext[b], unit_begin(k));
+            wait_vmem<0>();   // the tile has landed in LDS
+            wait_lgkm();
+            if (lane == 0) lds_store(&sLanded[b], k + 1);
+        }
+        wait_vmem<0>();   // no copy into LDS may outlive the workgroup
+        return;
+    }
+
+    // The wave's work is a stream of blocks: each unit it takes is cut into
+    // blocks of up to BLK entries.  A block is described by uniform values
+    // (entries [s, s + len) of col-group g, X slice at LDS float offset
+    // base, and whether it ends its unit).  While one block is multiplied,
+    // the loads of the next one are in flight; the two blocks live in two
+    // register sets used in turn, so nothing is copied between them.
+    //
+    // Every instruction issued next to the MFMAs costs SIMD time (a wave
+    // waiting to issue an MFMA holds the SIMD), so the per-block work is
+    // kept small: full blocks load with a scalar base and constant lane
+    // offsets, and lanes compute nothing else but their X row offsets.
+    struct Desc {
+        int32_t s, len, ze, base, g, slice;
+        bool last, valid;
+    };
+    struct Block {
+        int32_t ch;          // lane i < BLK: input channel of entry s + i
+        float av[STEPS];     // weight of step ks for this lane's (lane group, output)
+    };
+    // I and D are read through buffer resources: a scalar base per block, a
+    // constant lane offset and an immediate per step, so a block's loads cost
+    // no vector instructions; reads past the arrays return 0.  A block always
+    // loads BLK entries: entries past len belong to the next col-group (or
+    // are zeros past t) and meet the zero row of X.
+    const __amdgpu_buffer_rsrc_t rI =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.I), 0, a.t * 4, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rD =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.D), 0, a.t * N * 4, kBufferFlags);
+    const int lg = lane / N, lo = lane % N;
+    const int32_t lane_i = (lane % BLK) * 4, lane_d = lane * 4;
+    auto load_block = [&](Block& bk, const Desc& d) {
+        bk.ch = __builtin_amdgcn_raw_buffer_load_b32(rI, lane_i, d.s * 4, 0);
+#pragma unroll
+        for (int ks = 0; ks < STEPS; ++ks)
+            bk.av[ks] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, lane_d + ks * KS * N * 4, d.s * N * 4, 0));
+    };
+
+    acc_t acc[NB];
+#pragma unroll
+    for (int e = 0; e < NB; ++e)
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) acc[e][r] = 0.f;
+
+    // Multiplies one loaded block against X.  Lanes i >= len and channels
+    // outside [0, m) read the zero row.
+    const char* xs = reinterpret_cast<const char*>(sX + NB * lo);
+    auto run_block = [&](const Block& bk, const Desc& d) {
+        const bool ok = lane < d.len && bk.ch >= 0 && bk.ch < a.m;
+        const int32_t off = ok ? (d.base + bk.ch * PT) * 4 : ZERO_OFF;
+        vec_t bv[STEPS];
+#pragma unroll
+        for (int ks = 0; ks < STEPS; ++ks) {
+            const int32_t o = __builtin_amdgcn_ds_bpermute(4 * (ks * KS + lg), off);
+            bv[ks] = *reinterpret_cast<const vec_t*>(xs + o);
+        }
+        // Keep all X reads of the block ahead of the (guarded) MFMAs.
+#pragma unroll
+        for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(bv[ks]));
+        const int32_t nsteps = (d.len + KS - 1) / KS;
+        if (nsteps == STEPS) {
+#pragma unroll
+            for (int ks = 0; ks < STEPS; ++ks)
+#pragma unroll
+                for (int e = 0; e < NB; ++e) acc[e] = M::step(bk.av[ks], vec_el<NB>(bv[ks], e), acc[e]);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < STEPS; ++ks) {
+                if (ks >= nsteps) break;
+#pragma unroll
+                for (int e = 0; e < NB; ++e) acc[e] = M::step(bk.av[ks], vec_el<NB>(bv[ks], e), acc[e]);
+            }
+        }
+    };
+
+    // Stores the accumulators of a unit (or zeros, for a unit without kept
+    // blocks): MFMA (row, col n) of block e -> output channel g*N + row,
+    // pixel T*PT + slice*SW + NB*n + e.  Clears the accumulators.
+    float* __restrict__ y = static_cast<float*>(a.y);
+    auto store_unit = [&](int32_t tile, int32_t slice, int32_t g, bool zeros) {
+        const int32_t p0 = tile * PT + slice * SW + NB * lo;
+        if (kVec4) {
+            // HWo % 4 == 0: an aligned run of NB <= 4 pixels lies in one image.
+            if (p0 < a.npix) {
+                const int32_t b = p0 / a.HWo;
+                float* yb = y + int64_t(b) * a.y_img + (p0 - b * a.HWo);
+#pragma unroll
+                for (int r = 0; r < M::ACC; ++r) {
+                    const int32_t o = g * N + M::row(lane, r);
+                    if (o >= a.n) continue;
+                    vec_t v;
+#pragma unroll
+                    for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, zeros ? 0.f : acc[e][r]);
+                    *reinterpret_cast<vec_t*>(yb + int64_t(o) * a.y_c) = v;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < NB; ++e) {
+                const int32_t p = p0 + e;
+                if (p >= a.npix) continue;
+                const int32_t b = p / a.HWo;
+                const int64_t yb = int64_t(b) * a.y_img + (p - b * a.HWo);
+#pragma unroll
+                for (int r = 0; r < M::ACC; ++r) {
+                    const int32_t o = g * N + M::row(lane, r);
+                    if (o < a.n) y[yb + int64_t(o) * a.y_c] = zeros ? 0.f : acc[e][r];
+                }
+            }
+        }
+        if (!zeros) {
+#pragma unroll
+            for (int e = 0; e < NB; ++e)
+#pragma unroll
+                for (int r = 0; r < M::ACC; ++r) acc[e][r] = 0.f;
+        }
+    };
+
+    for (int32_t k = 0; k < ntiles; ++k) {
+        const int b = k & 1;
+        const int32_t T = T0 + k, ue = unit_end(k);
+        while (__builtin_amdgcn_readfirstlane(lds_load(&sLanded[b])) < k + 1)
+            __builtin_amdgcn_s_sleep(1);
+
+        // Units of this tile, taken from the LDS counter; a unit without
+        // kept blocks is stored as zeros right away.
+        auto next_unit = [&](Desc& d) {
+            while (true) {
+                int32_t u = 0;
+                if (lane == 0) u = atomicAdd(&sNext[b], 1);
+                u = __builtin_amdgcn_readfirstlane(u);
+                if (u >= ue) {
+                    d.valid = false;
+                    return;
+                }
+                const int32_t slice = SL == 1 ? 0 : __builtin_amdgcn_readfirstlane(u / G);
+                const int32_t g = u - slice * G;
+                const int32_t zb = __builtin_amdgcn_readfirstlane(sP[g] - g);
+                const int32_t ze = max(zb, __builtin_amdgcn_readfirstlane(sP[g + 1] - g - 1));
+                if (zb < ze) {
+                    d.s = zb;
+                    d.ze = ze;
+                    d.len = min(BLK, ze - zb);
+                    d.last = ze - zb <= BLK;
+                    d.base = b * kTileBufFloats + slice * SW;
+                    d.g = g;
+                    d.slice = slice;
+                    d.valid = true;
+                    return;
+                }
+                store_unit(T, slice, g, true);
+            }
+        };
+        auto advance = [&](const Desc& d) {
+            Desc r = d;
+            if (!d.last) {
+                r.s = d.s + d.len;
+                r.len = min(BLK, d.ze - r.s);
+                r.last = r.s + r.len >= d.ze;
+                return r;
+            }
+            next_unit(r);
+            return r;
+        };
+        // Runs block x (descriptor dx) while block y (descriptor dy = the
+        // one after dx) loads; returns the descriptor after dy.
+        auto step = [&](Block& x, const Desc& dx, Block& nb, Desc& dy) {
+            if (dy.valid) load_block(nb, dy);
+            run_block(x, dx);
+            // The next block's loads stay in flight across this block's MFMAs.
+            asm volatile("" : "+v"(nb.ch));
+#pragma unroll
+            for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(nb.av[ks]));
+            if (dx.last) store_unit(T, dx.slice, dx.g, false);
+        };
+
+        Desc d0;
+        next_unit(d0);
+        if (d0.valid) {
+            Block A, B;
+            load_block(A, d0);
+            Desc d1 = advance(d0);
+            while (true) {
+                step(A, d0, B, d1);
+                if (!d1.valid) break;
+                d0 = advance(d1);
+                step(B, d1, A, d0);
+                if (!d0.valid) break;
+                d1 = advance(d0);
+            }
+        }
+        // Every X read of this tile by this wave has completed (its MFMAs
+        // consumed them); release the buffer.
+        wait_lgkm();
+        if (lane == 0) atomicAdd(&sDone[b], 1);
+    }
+}
+
+// Slice width and slices per tile for a layer, or 0 when the resident-tile
+// kernel does not apply: the whole tile (m rows) must fit one 64 KB buffer,
+// a tile must hold at least 8 units so that few waves idle, and the total
+// cost must stay below 2^31.
+struct TileShape {
+    int sw, sl;
+};
+TileShape tile_shape(const ConvArgs& a) {
+    if (a.G > kTileMaxG) return {0, 0};
+    for (int sw : {64, 32, 16}) {
+        if (sw < (a.N == 32 ? 32 : 16)) continue;
+        if (int64_t(a.m) * sw > kTileBufFloats) continue;
+        int sl = 1;
+        while (int64_t(a.m) * sw * sl * 2 <= kTileBufFloats && int64_t(sl) * sw < a.npix && sl < 64)
+            sl *= 2;
+        if (int64_t(sl) * a.G < 8) continue;
+        const int64_t tiles = (int64_t(a.npix) + int64_t(sw) * sl - 1) / (int64_t(sw) * sl);
+        if (tiles * sl * (int64_t(a.t) + a.G) >= INT32_MAX) continue;
+        return {sw, sl};
+    }
+    return {0, 0};
+}
+
+bool vec4_ok(const ConvArgs& a) {
+    return a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
+           (reinterpret_cast<uintptr_t>(a.y) & 15) == 0;
+}
+
+template <int N, int SW>
+onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
+    const int64_t pt = int64_t(SW) * a.slices;
+    const int64_t tiles = (int64_t(a.npix) + pt - 1) / pt;
+    int64_t wgs = device_cu_count();
+    if (const char* env = std::getenv("ONEXN_PW_WGS")) {
+        const long v = std::atol(env);
+        if (v >= 1) wgs = v;
+    }
+    // (at most 2^15 workgroups keeps cost_r * L within int32 in the kernel)
+    wgs = std::max<int64_t>(1, std::min<int64_t>({wgs, tiles * a.slices * a.G, int64_t(1) << 15}));
+    const int64_t total = tiles * a.slices * (int64_t(a.t) + a.G);
+    a.cost_q = int32_t(total / wgs);
+    a.cost_r = int32_t(total % wgs);
+    if (vec4_ok(a)) return launch_grid(pw_tile_f32<N, SW, true>, a, wgs, s, kTileThreads);
+    return launch_grid(pw_tile_f32<N, SW, false>, a, wgs, s, kTileThreads);
+}
+
+}  // namespace
+
+bool pw_tile_applies(const ConvArgs& a) {
+    return (a.N == 16 || a.N == 32) && tile_shape(a).sw > 0;
+}
+
+onexn_status launch_pw_tile(ConvArgs a, hipStream_t s) {
+    const TileShape ts = tile_shape(a);
+    a.slices = ts.sl;
+    if (a.N == 16) {
+        if (ts.sw == 64) return launch_tile_sw<16, 64>(a, s);
+        if (ts.sw == 32) return launch_tile_sw<16, 32>(a, s);
+        return launch_tile_sw<16, 16>(a, s);
+    }
+    if (ts.sw == 64) return launch_tile_sw<32, 64>(a, s);
+    return launch_tile_sw<32, 32>(a, s);
+}
+
+}  // namespace onexn

@@ -143,17 +143,31 @@ def test_edge_shapes_integer_exact(case):
     np.testing.assert_array_equal(y, ref)
 
 
-def test_malformed_bsr_is_safe():
-    """I entries outside [0, m) are skipped and P is clamped to [0, t]."""
-    w, x = workloads.gen_integer_layer(seed=4, cout=32, cin=6, k=1, batch=1, H=5)
-    layer = onexn.prepare_layer(w, 16, 0.5, False)
-    I = layer.I.clone()
-    I[0] = 1 << 20
-    P = layer.P.clone()
-    P[-1] = 1 << 30
-    y = onexn.conv2d_fwd(P, I, layer.D, 32, x.cuda())
+@pytest.mark.parametrize("k,N", [(1, 16), (1, 32), (3, 16), (1, 4)])
+def test_out_of_range_channels_are_skipped(k, N):
+    """Entries of I outside [0, m) contribute nothing (kept ascending, so the
+    rest of the col-group is unaffected); P is clamped to [0, t]."""
+    print(f"skip case k={k} N={N}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=9)
+    layer = onexn.prepare_layer(w, N, 0.5, False)
+    P, I, D = layer.P.cpu(), layer.I.cpu().clone(), layer.D.cpu().clone()
+    hi, lo = int(P[1]) - 1, int(P[1])          # last entry of group 0, first of group 1
+    I[hi], I[lo] = 1 << 20, -5
+    y = onexn.conv2d_fwd(layer.P, I.cuda(), layer.D, 4 * N, x.cuda(), 1, k // 2)
+    # Expected: the same arrays with those two entries' weights zeroed.
+    D0 = D.clone()
+    D0[hi] = 0
+    D0[lo] = 0
+    I0 = I.clone()
+    I0[hi], I0[lo] = 0, 0
+    ref = oracle.decode(x.double().numpy(), P.numpy(), I0.numpy(), D0.double().numpy(), 4 * N,
+                        (1, 1), (k // 2, k // 2))
+    np.testing.assert_array_equal(y.double().cpu().numpy(), ref)
+    Pbad = layer.P.clone()
+    Pbad[-1] = 1 << 30
+    y2 = onexn.conv2d_fwd(Pbad, layer.I, layer.D, 4 * N, x.cuda(), 1, k // 2)
     torch.cuda.synchronize()
-    assert torch.isfinite(y).all()
+    assert torch.isfinite(y2).all()
 
 
 def test_runs_on_a_side_stream():
@@ -257,15 +271,45 @@ def test_config3_mobilenet_v2_layer_sampled(li):
 @pytest.mark.parametrize("wpg", ["1", "2", "4", "8"])
 @pytest.mark.parametrize("N", [16, 32])
 def test_pointwise_variants_integer_exact(N, wpg, hw, monkeypatch):
-    """Every waves-per-col-group variant of the pointwise kernel: several
-    channel chunks with a ragged last one (m = 300 > the largest chunk), col-group
-    sets with a partial last set and a ragged last col-group, and p from dense
-    to nearly empty (col-groups with no entries in some chunks)."""
+    """Every waves-per-col-group variant of the streamed pointwise kernel:
+    several channel chunks with a ragged last one (m = 300 > the largest
+    chunk), col-group sets with a partial last set and a ragged last
+    col-group, and p from dense to nearly empty (col-groups with no entries in
+    some chunks)."""
+    monkeypatch.setenv("ONEXN_PW_KERNEL", "stream")
     monkeypatch.setenv("ONEXN_PW_WPG", wpg)
     n = 9 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=N, cout=n, cin=300, k=1, batch=2, H=hw[0], W=hw[1],
                                        wmax=1, xmax=2)
     for p in (0.0, 0.5, 0.95):
         y, _ = gpu_conv(w, x, N, p, True, 1, 0)
+        ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
+        np.testing.assert_array_equal(y, ref)
+
+
+@pytest.mark.parametrize("wgs", ["1", "5", "default"])
+@pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
+@pytest.mark.parametrize("m", [200, 400, 900], ids=["m200", "m400", "m900"])
+@pytest.mark.parametrize("groups", [10, 2], ids=["G10", "G2"])
+@pytest.mark.parametrize("N", [16, 32])
+def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
+    """The resident-tile pointwise kernel at each slice width (m = 200, 400,
+    900 select 64-, 32- and 16-pixel slices), several slices per tile (two
+    col-groups), a ragged last col-group and ragged pixel tail, pixel rows
+    that do and do not allow 16-byte copies, and workgroup counts that cut the
+    cost ranges inside tiles (1, 5 and the default)."""
+    monkeypatch.setenv("ONEXN_PW_KERNEL", "tile")
+    if wgs != "default":
+        monkeypatch.setenv("ONEXN_PW_WGS", wgs)
+    n = (groups - 1) * N + N // 2
+    w, x = workloads.gen_integer_layer(seed=N + m, cout=n, cin=m, k=1, batch=2, H=hw[0], W=hw[1],
+                                       wmax=1, xmax=2)
+    print(f"pw tile N={N} n={n} m={m} hw={hw} wgs={wgs}", flush=True)
+    for p in (0.0, 0.5, 0.95):
+        try:
+            y, _ = gpu_conv(w, x, N, p, True, 1, 0)
+        except onexn.OnexnError as e:
+            assert e.status == 5   # ONEXN_ERR_UNSUPPORTED: the tile kernel does not fit
+            pytest.skip("resident-tile kernel does not fit this shape")
         ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
         np.testing.assert_array_equal(y, ref)
