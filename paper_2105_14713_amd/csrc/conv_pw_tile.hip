@@ -24,8 +24,9 @@
 // behind its next weight load.  Compute waves take the units of the landed
 // tile from an LDS counter until none is left and go straight on to the next
 // tile, so no wave waits for the others at tile ends.  LDS flags order the
-// two sides: `landed` (the loader has a tile in a buffer, counter reset) and
-// `done` (compute waves finished with a buffer's tile, so it may be reused).
+// two sides: `ready` (a buffer's unit counter is reset for its next tile),
+// `landed` (that tile's X is in the buffer) and `done` (compute waves
+// finished with a buffer's tile, so it may be reused).
 //
 // A wave computes a unit as a dense contraction over the col-group's kept
 // blocks, taken in blocks of 8 MFMA steps: for each block it reads the I
@@ -48,7 +49,7 @@ namespace {
 constexpr int kTileCompute = 15;                        // compute waves
 constexpr int kTileThreads = 64 * (kTileCompute + 1);   // + the loader wave
 constexpr int kTileBufFloats = 16384;                   // one X tile buffer: 64 KB
-constexpr int kTileSteps = 8;                           // MFMA steps per block
+constexpr int kTileSteps = 4;                           // MFMA steps per block
 constexpr int kTileMaxG = 256;                          // col-groups a layer may have
 constexpr int32_t kBufferFlags = 0x00020000;            // buffer resource word 3: 32-bit raw data
 
@@ -73,7 +74,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 
     __shared__ __attribute__((aligned(16))) float sX[2 * kTileBufFloats + SW];
     __shared__ int32_t sP[kTileMaxG + 1];   // P[g] + g: cost of the units before group g
-    __shared__ int32_t sNext[2], sLanded[2], sDone[2];
+    __shared__ int32_t sNext[2], sReady[2], sLanded[2], sDone[2];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -139,6 +140,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     for (int i = tid; i <= G; i += kTileThreads) sP[i] = max(0, min(a.P[i], a.t)) + i;
     for (int i = tid; i < SW; i += kTileThreads) sX[2 * kTileBufFloats + i] = 0.f;
     if (tid < 2) {
+        sReady[tid] = 0;
         sLanded[tid] = 0;
         sDone[tid] = 0;
     }
@@ -185,34 +187,34 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
                 while (__builtin_amdgcn_readfirstlane(lds_load(&sDone[b])) < kTileCompute * (k / 2))
                     __builtin_amdgcn_s_sleep(2);
             }
-            if (k > 0 || Tfirst != T0) copy_tile(T0 + k, b);
+            // The units can be handed out before the tile lands: compute
+            // waves load their first blocks' weights and indices meanwhile.
             if (lane == 0) lds_store(&sNext[b], unit_begin(k));
-            wait_vmem<0>();   // the tile has landed in LDS
             wait_lgkm();
+            if (lane == 0) lds_store(&sReady[b], k + 1);
+            if (k > 0 || Tfirst != T0) copy_tile(T0 + k, b);
+            wait_vmem<0>();   // the tile has landed in LDS
             if (lane == 0) lds_store(&sLanded[b], k + 1);
         }
         wait_vmem<0>();   // no copy into LDS may outlive the workgroup
         return;
     }
 
-    // The wave's work is a stream of blocks: each unit it takes is cut into
-    // blocks of up to BLK entries.  A block is described by uniform values
-    // (entries [s, s + len) of col-group g, X slice at LDS float offset
-    // base, and whether it ends its unit).  While one block is multiplied,
-    // the loads of the next one are in flight; the two blocks live in two
-    // register sets used in turn, so nothing is copied between them.
-    //
-    // Every instruction issued next to the MFMAs costs SIMD time (a wave
-    // waiting to issue an MFMA holds the SIMD), so the per-block work is
-    // kept small: full blocks load with a scalar base and constant lane
-    // offsets, and lanes compute nothing else but their X row offsets.
+    // The wave's work in a tile is a stream of blocks: each unit it takes is
+    // cut into blocks of up to BLK entries (STEPS MFMA steps), described by
+    // uniform values (entries [s, s + len) of col-group g, X slice at LDS
+    // float offset base, whether it ends its unit).  The stream is
+    // software-pipelined: while block j is multiplied, the wave reads block
+    // j+1's X rows from LDS, hands block j+2's row offsets to its lane groups
+    // (ds_bpermute), and loads block j+1's weights and block j+3's channel
+    // indices.  These instructions are interleaved with block j's MFMAs
+    // because a wave waiting to issue an MFMA holds its SIMD: work issued
+    // between MFMAs is nearly free, work issued around a run of MFMAs is
+    // not.  Registers of consecutive blocks alternate between two sets (the
+    // loop is unrolled by two), so nothing is copied from block to block.
     struct Desc {
         int32_t s, len, ze, base, g, slice;
         bool last, valid;
-    };
-    struct Block {
-        int32_t ch;          // lane i < BLK: input channel of entry s + i
-        float av[STEPS];     // weight of step ks for this lane's (lane group, output)
     };
     // I and D are read through buffer resources: a scalar base per block, a
     // constant lane offset and an immediate per step, so a block's loads cost
@@ -225,11 +227,29 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
         __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.D), 0, a.t * N * 4, kBufferFlags);
     const int lg = lane / N, lo = lane % N;
     const int32_t lane_i = (lane % BLK) * 4, lane_d = lane * 4;
-    auto load_block = [&](Block& bk, const Desc& d) {
-        bk.ch = __builtin_amdgcn_raw_buffer_load_b32(rI, lane_i, d.s * 4, 0);
+    auto load_ch = [&](int32_t& ch, const Desc& d) {
+        ch = __builtin_amdgcn_raw_buffer_load_b32(rI, lane_i, d.s * 4, 0);
+    };
+    auto load_w = [&](float (&av)[STEPS], const Desc& d) {
 #pragma unroll
         for (int ks = 0; ks < STEPS; ++ks)
-            bk.av[ks] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, lane_d + ks * KS * N * 4, d.s * N * 4, 0));
+            av[ks] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, lane_d + ks * KS * N * 4, d.s * N * 4, 0));
+    };
+    // Row offsets of a block, one per step for this lane's group: lane i of
+    // the block names entry i's X row (lanes i >= len and channels outside
+    // [0, m) name the zero row); step ks hands entry ks*KS + lg's row to
+    // lane group lg.
+    auto offsets = [&](int32_t (&o)[STEPS], int32_t ch, const Desc& d) {
+        const int32_t row = (d.base + ch * PT) * 4;
+        const bool ok = lane < d.len && uint32_t(ch) < uint32_t(a.m);
+        const int32_t off = ok ? row : ZERO_OFF;
+#pragma unroll
+        for (int ks = 0; ks < STEPS; ++ks) o[ks] = __builtin_amdgcn_ds_bpermute(4 * (ks * KS + lg), off);
+    };
+    const char* xs = reinterpret_cast<const char*>(sX + NB * lo);
+    auto read_x = [&](vec_t (&bv)[STEPS], const int32_t (&o)[STEPS]) {
+#pragma unroll
+        for (int ks = 0; ks < STEPS; ++ks) bv[ks] = *reinterpret_cast<const vec_t*>(xs + o[ks]);
     };
 
     acc_t acc[NB];
@@ -237,37 +257,6 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     for (int e = 0; e < NB; ++e)
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) acc[e][r] = 0.f;
-
-    // Multiplies one loaded block against X.  Lanes i >= len and channels
-    // outside [0, m) read the zero row.
-    const char* xs = reinterpret_cast<const char*>(sX + NB * lo);
-    auto run_block = [&](const Block& bk, const Desc& d) {
-        const bool ok = lane < d.len && bk.ch >= 0 && bk.ch < a.m;
-        const int32_t off = ok ? (d.base + bk.ch * PT) * 4 : ZERO_OFF;
-        vec_t bv[STEPS];
-#pragma unroll
-        for (int ks = 0; ks < STEPS; ++ks) {
-            const int32_t o = __builtin_amdgcn_ds_bpermute(4 * (ks * KS + lg), off);
-            bv[ks] = *reinterpret_cast<const vec_t*>(xs + o);
-        }
-        // Keep all X reads of the block ahead of the (guarded) MFMAs.
-#pragma unroll
-        for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(bv[ks]));
-        const int32_t nsteps = (d.len + KS - 1) / KS;
-        if (nsteps == STEPS) {
-#pragma unroll
-            for (int ks = 0; ks < STEPS; ++ks)
-#pragma unroll
-                for (int e = 0; e < NB; ++e) acc[e] = M::step(bk.av[ks], vec_el<NB>(bv[ks], e), acc[e]);
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < STEPS; ++ks) {
-                if (ks >= nsteps) break;
-#pragma unroll
-                for (int e = 0; e < NB; ++e) acc[e] = M::step(bk.av[ks], vec_el<NB>(bv[ks], e), acc[e]);
-            }
-        }
-    };
 
     // Stores the accumulators of a unit (or zeros, for a unit without kept
     // blocks): MFMA (row, col n) of block e -> output channel g*N + row,
@@ -315,7 +304,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     for (int32_t k = 0; k < ntiles; ++k) {
         const int b = k & 1;
         const int32_t T = T0 + k, ue = unit_end(k);
-        while (__builtin_amdgcn_readfirstlane(lds_load(&sLanded[b])) < k + 1)
+        while (__builtin_amdgcn_readfirstlane(lds_load(&sReady[b])) < k + 1)
             __builtin_amdgcn_s_sleep(1);
 
         // Units of this tile, taken from the LDS counter; a unit without
@@ -349,6 +338,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
         };
         auto advance = [&](const Desc& d) {
             Desc r = d;
+            if (!d.valid) return r;
             if (!d.last) {
                 r.s = d.s + d.len;
                 r.len = min(BLK, d.ze - r.s);
@@ -358,31 +348,70 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
             next_unit(r);
             return r;
         };
-        // Runs block x (descriptor dx) while block y (descriptor dy = the
-        // one after dx) loads; returns the descriptor after dy.
-        auto step = [&](Block& x, const Desc& dx, Block& nb, Desc& dy) {
-            if (dy.valid) load_block(nb, dy);
-            run_block(x, dx);
-            // The next block's loads stay in flight across this block's MFMAs.
-            asm volatile("" : "+v"(nb.ch));
+
+        // One pipeline step: multiply block j (d0: weights av0, X bv0) while
+        // reading block j+1's X (offsets o1) into bv1, handing out block
+        // j+2's row offsets (d2, channels ch2) into o2, and loading block
+        // j+1's weights (d1) into av1 and block j+3's channels (d3) into
+        // ch3.  Work for a missing block redoes block j, so that every step
+        // issues the same instructions (one straight run the scheduler can
+        // interleave) and the waits for loads stay exact.
+        auto step = [&](const Desc& d0, const Desc& d1, const Desc& d2, const Desc& d3,
+                        float (&av0)[STEPS], vec_t (&bv0)[STEPS], float (&av1)[STEPS],
+                        vec_t (&bv1)[STEPS], const int32_t (&o1)[STEPS], int32_t (&o2)[STEPS],
+                        int32_t ch2, int32_t& ch3) {
+            load_ch(ch3, d3.valid ? d3 : d0);
+            load_w(av1, d1.valid ? d1 : d0);
+            offsets(o2, ch2, d2.valid ? d2 : d0);
+            read_x(bv1, o1);
 #pragma unroll
-            for (int ks = 0; ks < STEPS; ++ks) asm volatile("" : "+v"(nb.av[ks]));
-            if (dx.last) store_unit(T, dx.slice, dx.g, false);
+            for (int ks = 0; ks < STEPS; ++ks)
+#pragma unroll
+                for (int e = 0; e < NB; ++e) acc[e] = M::step(av0[ks], vec_el<NB>(bv0[ks], e), acc[e]);
+#pragma unroll
+            for (int i = 0; i < STEPS * NB; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA,
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // a load,
+                __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);   // a vector op
+                __builtin_amdgcn_sched_group_barrier(0x080, 1, 0);   // and an LDS op
+            }
+            if (d0.last) store_unit(T, d0.slice, d0.g, false);
         };
 
         Desc d0;
         next_unit(d0);
         if (d0.valid) {
-            Block A, B;
-            load_block(A, d0);
             Desc d1 = advance(d0);
+            Desc d2 = advance(d1);
+            Desc d3 = advance(d2);
+            int32_t chA, chB, oA[STEPS], oB[STEPS];
+            float avA[STEPS], avB[STEPS];
+            vec_t bvA[STEPS], bvB[STEPS];
+            // Prologue: blocks 0 and 1's offsets, block 0's weights and X,
+            // block 2's channels (block j's registers use set j % 2).
+            load_ch(chA, d0);
+            load_ch(chB, d1.valid ? d1 : d0);
+            load_w(avA, d0);
+            offsets(oA, chA, d0);
+            offsets(oB, chB, d1.valid ? d1 : d0);
+            load_ch(chA, d2.valid ? d2 : d0);
+            // Only the X reads need the tile itself.
+            while (__builtin_amdgcn_readfirstlane(lds_load(&sLanded[b])) < k + 1)
+                __builtin_amdgcn_s_sleep(1);
+            read_x(bvA, oA);
             while (true) {
-                step(A, d0, B, d1);
+                step(d0, d1, d2, d3, avA, bvA, avB, bvB, oB, oA, chA, chB);
                 if (!d1.valid) break;
-                d0 = advance(d1);
-                step(B, d1, A, d0);
-                if (!d0.valid) break;
-                d1 = advance(d0);
+                d0 = d1;
+                d1 = d2;
+                d2 = d3;
+                d3 = advance(d3);
+                step(d0, d1, d2, d3, avB, bvB, avA, bvA, oA, oB, chB, chA);
+                if (!d1.valid) break;
+                d0 = d1;
+                d1 = d2;
+                d2 = d3;
+                d3 = advance(d3);
             }
         }
         // Every X read of this tile by this wave has completed (its MFMAs
