@@ -74,7 +74,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 
     __shared__ __attribute__((aligned(16))) float sX[2 * kTileBufFloats + SW];
     __shared__ int32_t sP[kTileMaxG + 1];   // P[g] + g: cost of the units before group g
-    __shared__ int32_t sNext[2], sReady[2], sLanded[2], sDone[2];
+    __shared__ int32_t sNext[2], sReady[2], sLanded[2], sDone[2], sSetup;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -136,16 +136,39 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 
     const bool loader = wave == kTileCompute;
     const int32_t Tfirst = c0 / tile_cost;
-    if (loader) copy_tile(Tfirst, 0);   // started before anything else
-    for (int i = tid; i <= G; i += kTileThreads) sP[i] = max(0, min(a.P[i], a.t)) + i;
-    for (int i = tid; i < SW; i += kTileThreads) sX[2 * kTileBufFloats + i] = 0.f;
     if (tid < 2) {
         sReady[tid] = 0;
         sLanded[tid] = 0;
         sDone[tid] = 0;
     }
+    if (tid == 0) sSetup = 0;
     wait_lgkm();
-    __builtin_amdgcn_s_barrier();   // sP and the flags are set
+    __builtin_amdgcn_s_barrier();   // the flags are set (all waves arrive at once)
+
+    // The loader starts the first tile's copy right away.  The compute waves
+    // meanwhile put P into LDS through the scalar cache (each wave loads
+    // chunks of 16 entries with uniform addresses clamped to the array) and
+    // meet on an LDS counter, not a barrier, so that none of them waits for
+    // the loader to finish issuing the copy.
+    if (loader) {
+        copy_tile(Tfirst, 0);
+    } else {
+        for (int32_t c = wave; c * 16 <= G; c += kTileCompute) {
+            int32_t v = 0;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int32_t pj = a.P[min(c * 16 + j, G)];
+                v = lane == j ? pj : v;
+            }
+            const int32_t i = c * 16 + lane;
+            if (lane < 16 && i <= G) sP[i] = max(0, min(v, a.t)) + i;
+        }
+        for (int i = lane; i < SW; i += 64)
+            if (wave == 0) sX[2 * kTileBufFloats + i] = 0.f;
+        wait_lgkm();
+        if (lane == 0) atomicAdd(&sSetup, 1);
+    }
+    while (__builtin_amdgcn_readfirstlane(lds_load(&sSetup)) < kTileCompute) __builtin_amdgcn_s_sleep(1);
 
     // First unit at or after cost offset c: the tile's units sorted by
     // start cost s*(t + G) + P[g] + g.
@@ -179,6 +202,12 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     auto unit_begin = [&](int32_t k) { return k == 0 ? u0 : 0; };
     auto unit_end = [&](int32_t k) { return T0 + k == T1 ? u1 : units; };
 
+    if (wave == 0 && ntiles > 0) {
+        if (lane == 0) lds_store(&sNext[0], unit_begin(0));
+        wait_lgkm();
+        if (lane == 0) lds_store(&sReady[0], 1);
+    }
+
     if (loader) {
         for (int32_t k = 0; k < ntiles; ++k) {
             const int b = k & 1;
@@ -189,9 +218,12 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
             }
             // The units can be handed out before the tile lands: compute
             // waves load their first blocks' weights and indices meanwhile.
-            if (lane == 0) lds_store(&sNext[b], unit_begin(k));
-            wait_lgkm();
-            if (lane == 0) lds_store(&sReady[b], k + 1);
+            // (The first tile's counter is set by compute wave 0.)
+            if (k > 0) {
+                if (lane == 0) lds_store(&sNext[b], unit_begin(k));
+                wait_lgkm();
+                if (lane == 0) lds_store(&sReady[b], k + 1);
+            }
             if (k > 0 || Tfirst != T0) copy_tile(T0 + k, b);
             wait_vmem<0>();   // the tile has landed in LDS
             if (lane == 0) lds_store(&sLanded[b], k + 1);
