@@ -161,6 +161,8 @@ bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onex
 onexn_status launch_pointwise(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
 bool pw_tile_applies(const ConvArgs& a);
 onexn_status launch_pw_tile(ConvArgs a, hipStream_t stream);
+bool pw_bf16_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_pw_bf16(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
 
 // Launches `kernel` on a 1-D grid of `total` workgroups.
 template <typename K>

@@ -1,0 +1,463 @@
+// Pointwise (1x1, stride 1, no padding, NCHW) 1xN-pruned convolution with
+// bf16 inputs and weights, fp32 accumulation, N = 32, bf16 or fp32 output.
+//
+// Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
+// (arXiv 2105.14713), Sec. 3.4, Eq. 8.  Col-group g is the contraction
+//     Y_g[32][pixels] = D_g^T[32][kept_g] * X[I_g][pixels]:
+// its kept blocks select rows of the input matrix X[channel][pixel].
+//
+// Matrix cores.  v_mfma_f32_32x32x16_bf16 multiplies a 32x16 A fragment (the
+// 32 weights of 16 kept blocks) by a 16x32 B fragment (16 gathered input rows
+// at 32 pixels); each lane holds 8 consecutive contraction entries of one
+// output row (A) or one pixel (B).  For a 1xN layer those 8 entries are 8
+// kept channels, i.e. 8 different rows of X, so B cannot be read with plain
+// vector loads.  gfx950's ds_read_b64_tr_b16 does exactly this transposition:
+// each lane names the row it wants (any row) and receives the 16-bit
+// elements of four lanes' rows.  The same instruction transposes the weight
+// panel D (stored with the 32 outputs of a block contiguous) into the A
+// fragment.
+//
+// Work split.  A work item is (pixel tile of 128 columns, set of 8
+// col-groups); each of the workgroup's 8 compute waves computes one col-group
+// over the tile (32 x 128 fp32 accumulators).  A pixel tile is 16 granules of
+// 8 pixels; a granule lies in one image (the last granule of an image may be
+// partial), so that each granule of a channel is one 16-byte copy.
+//
+// Input staging.  The workgroup's ninth wave copies X into LDS in chunks of 64
+// channels x 128 columns (16 KB) with buffer loads straight into LDS, into a
+// ring of 3 chunk buffers, as far ahead as the ring allows.  Rows are stored
+// with their four 64-byte column blocks rotated by (row mod 4), so that the 8
+// rows one transposed read touches spread over the LDS banks.  LDS counters,
+// not barriers, order the two sides: `landed` counts chunks in LDS, each
+// compute wave's `need` is the first chunk it may still read; a buffer is
+// refilled once every wave's `need` has passed the chunk in it.
+//
+// Kept blocks.  A compute wave walks its col-group's kept blocks in steps of
+// up to 16 (one MFMA k-step): a step takes the next 16 blocks unless their
+// channels span more than the 3 chunks the ring holds, in which case it stops
+// short.  The blocks' weights (16 x 64 bytes) and channel indices are copied
+// into a per-wave LDS ring in windows of 16 blocks, up to 5 windows ahead.
+// Steps are software-pipelined: while step j's four MFMAs run, the wave reads
+// step j+1's A and B fragments and step j+2's channel indices.  Entries past
+// a step's end, and channels outside [0, m), read a zero row for both A and
+// B, so they add exactly nothing.
+#include <cstdlib>
+
+#include "pw_common.h"
+
+namespace onexn {
+namespace {
+
+constexpr int kQWaves = 8;                       // compute waves, one col-group each
+constexpr int kQThreads = 64 * (kQWaves + 1);    // + the loader wave
+constexpr int kQKcShift = 6;
+constexpr int kQKc = 1 << kQKcShift;             // input channels per X chunk
+constexpr int kQRing = 3;                        // X chunk buffers
+constexpr int kQGran = 16;                       // 8-pixel granules per tile
+constexpr int kQCols = 8 * kQGran;               // pixel columns per tile
+constexpr int kQBlocks = kQCols / 32;            // MFMA column blocks
+constexpr int kQRowB = kQCols * 2;               // bytes per X row in LDS
+constexpr int kQBufB = kQKc * kQRowB;            // bytes per chunk buffer
+constexpr int kQCopies = kQBufB / 1024;          // 1 KB copies per chunk
+constexpr int kQZeroOff = kQRing * kQBufB;       // a row of zeros after the ring
+constexpr int kQWin = 16;                        // kept blocks per window (one k-step)
+constexpr int kQWins = 8;                        // windows in a wave's ring
+constexpr int kQRingE = kQWin * kQWins;          // ring entries
+constexpr int kQARowB = 64;                      // bytes of one block's weights (32 bf16)
+constexpr int32_t kQNever = 0x3fffffff;
+constexpr int32_t kQBufferFlags = 0x00020000;    // buffer resource word 3: 32-bit raw data
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+__device__ __forceinline__ int32_t lds_load(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_store(int32_t* p, int32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+// Compiler-only barrier: no memory access moves across it.
+__device__ __forceinline__ void fence_compiler() { asm volatile("" ::: "memory"); }
+
+__device__ __forceinline__ v4i16 tr_read(const lds_char* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p);
+}
+
+__device__ __forceinline__ bf16x8 join(v4i16 lo, v4i16 hi) {
+    const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Raw buffer resource over [p, p + bytes): reads past the end return zeros.
+__device__ __forceinline__ v4i32 buffer_rsrc(const void* p, int32_t bytes) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    v4i32 r;
+    r.x = __builtin_amdgcn_readfirstlane(int32_t(uint32_t(v)));
+    r.y = __builtin_amdgcn_readfirstlane(int32_t(uint32_t(v >> 32) & 0xffff));
+    r.z = __builtin_amdgcn_readfirstlane(bytes);
+    r.w = kQBufferFlags;
+    return r;
+}
+
+// (m0 is named as clobbered for the reader; the compiler keeps nothing in it here.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// Copies from a buffer straight into LDS: lane i's 16 (or 4) bytes at byte
+// offset voff + soff land at LDS address dst + 16 i (4 i).  Written as inline
+// assembly so that the compiler, which cannot tell which LDS bytes such a copy
+// writes, does not make every later LDS read wait for all outstanding copies;
+// the kernel orders them itself with the waits below.
+__device__ __forceinline__ void copy16_to_lds(v4i32 rs, const lds_char* dst, int32_t voff, int32_t soff) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(dst)));
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
+}
+__device__ __forceinline__ void copy4_to_lds(v4i32 rs, const lds_char* dst, int32_t voff, int32_t soff) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(dst)));
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
+}
+
+#pragma clang diagnostic pop
+
+// Waits until at most N vector-memory instructions of this wave are
+// outstanding; also a compiler barrier for memory accesses.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+// Waits until at most n (even) copies are outstanding; n is wave-uniform.
+__device__ __forceinline__ void vm_wait_upto(int32_t n) {
+    if (n <= 0) vm_wait<0>();
+    else if (n == 2) vm_wait<2>();
+    else if (n == 4) vm_wait<4>();
+    else if (n == 6) vm_wait<6>();
+    else if (n == 8) vm_wait<8>();
+    else if (n == 10) vm_wait<10>();
+    else if (n == 12) vm_wait<12>();
+    else vm_wait<14>();
+}
+
+// One k-step of a col-group: entries [rz, rz + len) (relative to the group's
+// first block) whose valid channels lie in chunk sequence numbers [smin, smax]
+// (smin < 0: no valid channel).
+struct QStep {
+    int32_t rz, len, smin, smax;
+};
+
+template <typename TY>
+__global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
+    __shared__ __attribute__((aligned(16))) char sX[kQRing * kQBufB + kQRowB];
+    __shared__ __attribute__((aligned(16))) char sA[kQWaves * kQRingE * kQARowB];
+    __shared__ __attribute__((aligned(16))) int32_t sI[kQWaves * kQRingE];
+    __shared__ int32_t sNeed[kQWaves];
+    __shared__ int32_t sLanded;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t batch = a.npix / a.HWo;
+    const int32_t gpi = (a.HWo + 7) >> 3;                 // granules per image
+    const int32_t ngran = batch * gpi;
+    const int32_t ntiles = (ngran + kQGran - 1) / kQGran;
+    const int32_t gsets = (a.G + kQWaves - 1) / kQWaves;
+    const int32_t nitems = ntiles * gsets;
+    const int32_t nchunks = (a.m + kQKc - 1) >> kQKcShift;
+    const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
+    const int32_t nloc = L < nitems ? (nitems - 1 - L) / a.total + 1 : 0;   // items of this workgroup
+
+    for (int i = tid; i < kQRowB / 4; i += kQThreads) reinterpret_cast<int32_t*>(sX + kQZeroOff)[i] = 0;
+    if (tid < kQWaves) sNeed[tid] = 0;
+    if (tid == 0) sLanded = 0;
+    __syncthreads();
+
+    const lds_char* const lx = (const lds_char*)sX;
+
+    if (wave == kQWaves) {
+        // ---- Loader wave: chunk sequence number s = k * nchunks + c (the
+        // workgroup's item k, channel chunk c) goes to buffer s % 3.
+        const v4i32 rX = buffer_rsrc(a.x, int32_t(int64_t(batch) * a.x_img * 2));
+        const int h = lane >> 4, q = lane & 15;            // row within a copy (= its rotation), slot
+        const int32_t gran = 4 * (((q >> 2) - h) & 3) + (q & 3);   // tile granule held by slot q
+        const int32_t rowb = a.HWo * 2;                    // bytes between channels
+        const int32_t total_seq = nloc * nchunks;
+        int32_t pbase = 0, cur_k = -1;
+        auto issue = [&](int32_t s) {
+            const int32_t k = s / nchunks, c = s - k * nchunks;
+            if (k != cur_k) {
+                cur_k = k;
+                const int32_t tile = (L + k * a.total) / gsets;
+                const int32_t id = tile * kQGran + gran;
+                pbase = 0;
+                if (id < ngran) {
+                    const int32_t b = id / gpi, j = id - b * gpi;
+                    pbase = int32_t(int64_t(b) * a.x_img * 2) + 16 * j;
+                }
+            }
+            const lds_char* dst = lx + (s % kQRing) * kQBufB;
+            const int32_t ch0 = c * kQKc + h;
+#pragma unroll 4
+            for (int i = 0; i < kQCopies; ++i) {
+                const int32_t ch = min(ch0 + 4 * i, a.m - 1);   // rows past m copy a real row (never read)
+                copy16_to_lds(rX, dst + i * 1024, pbase + ch * rowb, 0);
+            }
+        };
+        auto min_need = [&]() {
+            const int32_t v = lane < kQWaves ? lds_load(&sNeed[lane]) : kQNever;
+            int32_t mn = kQNever;
+#pragma unroll
+            for (int w = 0; w < kQWaves; ++w) mn = min(mn, __builtin_amdgcn_readlane(v, w));
+            return mn;
+        };
+        int32_t issued = 0, landed = 0;
+        while (landed < total_seq) {
+            if (issued < total_seq && issued - landed < 2) {
+                if (min_need() >= issued - (kQRing - 1)) {
+                    issue(issued);
+                    ++issued;
+                    continue;
+                }
+                if (issued == landed) {
+                    __builtin_amdgcn_s_sleep(1);
+                    continue;
+                }
+            }
+            if (issued - landed == 2) vm_wait<kQCopies>();
+            else vm_wait<0>();
+            ++landed;
+            if (lane == 0) lds_store(&sLanded, landed);
+        }
+        vm_wait<0>();   // no copy into LDS may outlive the workgroup
+        return;
+    }
+
+    // ---- Compute waves.
+    const int w = wave;
+    const lds_char* const myA = (const lds_char*)sA + w * (kQRingE * kQARowB);
+    const int32_t* const myI = sI + w * kQRingE;
+    const lds_char* const zrow = lx + kQZeroOff;
+    // Lane roles of a transposed read: lane l names entry k1 (k1 + 4 for the
+    // second read) at 4 consecutive columns starting at byte colb of a 64-byte
+    // block (the same roles serve the A and the B fragment).
+    const int k1 = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    const int colb = 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
+    TY* __restrict__ y = static_cast<TY*>(a.y);
+
+    f32x16 acc[kQBlocks];
+    int32_t need = 0;
+    for (int32_t k = 0; k < nloc; ++k) {
+        const int32_t item = L + k * a.total;
+        const int32_t tile = item / gsets;
+        const int32_t g = (item - tile * gsets) * kQWaves + w;
+        const int32_t seq_base = k * nchunks;
+#pragma unroll
+        for (int e = 0; e < kQBlocks; ++e)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[e][r] = 0.f;
+
+        int32_t zb = 0, ze = 0;
+        if (g < a.G) group_range(a, g, zb, ze);
+        const int32_t nE = ze - zb;
+        if (nE > 0) {
+            const int32_t nwin = (nE + kQWin - 1) / kQWin;
+            const v4i32 rA = buffer_rsrc(a.D, ze * kQARowB);
+            const v4i32 rI = buffer_rsrc(a.I, ze * 4);
+            int32_t wi = 0;   // windows issued
+            auto issue_windows = [&](int32_t upto) {   // windows [wi, min(upto, nwin))
+                upto = min(upto, nwin);
+                for (; wi < upto; ++wi) {
+                    const int32_t slot = wi % kQWins;
+                    copy16_to_lds(rA, myA + slot * (kQWin * kQARowB), lane * 16, (zb + wi * kQWin) * kQARowB);
+                    if (lane < kQWin)
+                        copy4_to_lds(rI, (const lds_char*)myI + slot * (kQWin * 4), lane * 4, (zb + wi * kQWin) * 4);
+                }
+            };
+            // Waits until the windows holding entries rz .. rz + 15 have landed.
+            auto wait_windows = [&](int32_t rz) {
+                const int32_t wneed = min((rz + kQWin - 1) / kQWin + 1, nwin) - 1;
+                vm_wait_upto(2 * (wi - 1 - wneed));
+            };
+            // Channel indices for the step at rz: pl (lanes < 16: entry rz +
+            // lane), o1 / o2 (entry rz + k1 / rz + k1 + 4).
+            auto plan_reads = [&](int32_t rz, int32_t& pl, int32_t& o1, int32_t& o2) {
+                pl = myI[(rz + (lane & 15)) & (kQRingE - 1)];
+                o1 = myI[(rz + k1) & (kQRingE - 1)];
+                o2 = myI[(rz + k1 + 4) & (kQRingE - 1)];
+            };
+            auto plan = [&](int32_t rz, int32_t pl) {
+                QStep st;
+                st.rz = rz;
+                const bool inE = lane < kQWin && rz + lane < nE;
+                const bool okc = inE && pl >= 0 && pl < a.m;
+                const int32_t sq = okc ? seq_base + (pl >> kQKcShift) : -1;
+                const int32_t avail = __builtin_popcountll(__ballot(inE));
+                const uint64_t mv = __ballot(okc);
+                if (mv == 0) {
+                    st.len = avail;
+                    st.smin = st.smax = -1;
+                    return st;
+                }
+                st.smin = __builtin_amdgcn_readlane(sq, __builtin_ctzll(mv));
+                const uint64_t far = __ballot(okc && sq > st.smin + (kQRing - 1));
+                st.len = min(avail, far ? int32_t(__builtin_ctzll(far)) : 64);
+                const bool in_step = okc && lane < st.len;
+                st.smax = __ballot(in_step && sq == st.smin + 2) ? st.smin + 2
+                        : __ballot(in_step && sq == st.smin + 1) ? st.smin + 1
+                        : st.smin;
+                return st;
+            };
+            // LDS addresses of one lane's entry (k1 + 4 hh) for a step: its A
+            // row and its X row (column blocks rotated by rot), or the zero row.
+            struct Addr {
+                const lds_char* ap;
+                int32_t xoff, rot;
+            };
+            auto addr = [&](const QStep& st, int32_t ch, int hh) {
+                Addr r;
+                const int32_t e = k1 + 4 * hh;
+                const bool ok = e < st.len && ch >= 0 && ch < a.m;
+                const int32_t row = ch & (kQKc - 1);
+                r.xoff = ok ? ((seq_base + (ch >> kQKcShift)) % kQRing) * kQBufB + row * kQRowB + colb
+                            : kQZeroOff + colb;
+                r.rot = ok ? (row & 3) : 0;
+                r.ap = ok ? myA + ((st.rz + e) & (kQRingE - 1)) * kQARowB + colb : zrow + colb;
+                return r;
+            };
+            auto wait_landed = [&](const QStep& st) {
+                if (st.smax >= 0)
+                    while (__builtin_amdgcn_readfirstlane(lds_load(&sLanded)) <= st.smax)
+                        __builtin_amdgcn_s_sleep(1);
+                fence_compiler();
+            };
+            auto release = [&](const QStep& st) {
+                if (st.smin > need) {
+                    need = st.smin;
+                    if (lane == 0) lds_store(&sNeed[w], need);
+                }
+            };
+
+            // Prologue: step 0 planned and its fragments read; step 1's indices read.
+            issue_windows(kQWins - 3);
+            wait_windows(0);
+            int32_t pl, o1, o2;
+            plan_reads(0, pl, o1, o2);
+            wait_lgkm();
+            QStep cur = plan(0, pl);
+            release(cur);
+            wait_landed(cur);
+            v4i16 ra[2], rb[kQBlocks][2];
+            {
+                const Addr p1 = addr(cur, o1, 0), p2 = addr(cur, o2, 1);
+                ra[0] = tr_read(p1.ap);
+                ra[1] = tr_read(p2.ap);
+#pragma unroll
+                for (int blk = 0; blk < kQBlocks; ++blk) {
+                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * ((blk + p1.rot) & 3));
+                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * ((blk + p2.rot) & 3));
+                }
+            }
+            int32_t rz_next = cur.len;
+            if (rz_next < nE) {
+                wait_windows(rz_next);
+                plan_reads(rz_next, pl, o1, o2);
+            }
+
+            // Step j: multiply the fragments in (ra, rb); plan step j+1 from
+            // (pl, o1, o2) and read its fragments into (ra, rb) as each of
+            // step j's MFMAs takes its operands; read step j+2's indices.
+            while (true) {
+                wait_lgkm();
+                const bool has_next = rz_next < nE;
+                QStep nxt = plan(rz_next, pl);
+                if (!has_next) nxt.len = 0;
+                if (has_next) {
+                    release(nxt);
+                    issue_windows(rz_next / kQWin + kQWins - 1);
+                    wait_landed(nxt);
+                }
+                const int32_t rz2 = rz_next + nxt.len;
+                const bool has_next2 = has_next && rz2 < nE;
+                const Addr p1 = addr(nxt, o1, 0), p2 = addr(nxt, o2, 1);
+                const bf16x8 af = join(ra[0], ra[1]);
+                ra[0] = tr_read(p1.ap);
+                ra[1] = tr_read(p2.ap);
+#pragma unroll
+                for (int blk = 0; blk < kQBlocks; ++blk) {
+                    acc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, join(rb[blk][0], rb[blk][1]),
+                                                                     acc[blk], 0, 0, 0);
+                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * ((blk + p1.rot) & 3));
+                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * ((blk + p2.rot) & 3));
+                }
+                if (has_next2) {
+                    wait_windows(rz2);
+                    plan_reads(rz2, pl, o1, o2);
+                }
+                if (!has_next) break;
+                rz_next = rz2;
+            }
+            wait_lgkm();
+        }
+        // Past this item's chunks.
+        if (seq_base + nchunks > need) {
+            need = seq_base + nchunks;
+            if (lane == 0) lds_store(&sNeed[w], need);
+        }
+
+        // Store: MFMA (row, col) of block e -> output channel g*32 + row, tile column 32e + col.
+        if (g < a.G) {
+#pragma unroll
+            for (int e = 0; e < kQBlocks; ++e) {
+                const int32_t n = 32 * e + (lane & 31);
+                const int32_t id = tile * kQGran + (n >> 3);
+                const int32_t b = id / gpi;
+                const int32_t hw = 8 * (id - b * gpi) + (n & 7);
+                if (id >= ngran || hw >= a.HWo) continue;
+                TY* yb = y + int64_t(b) * a.y_img + hw;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int32_t o = g * 32 + PwMfma<32>::row(lane, r);
+                    if (o < a.n) yb[int64_t(o) * a.y_c] = from_f32<TY>(acc[e][r]);
+                }
+            }
+        }
+    }
+    if (lane == 0) lds_store(&sNeed[w], kQNever);
+}
+
+template <typename TY>
+onexn_status launch_typed(ConvArgs a, hipStream_t s) {
+    const int64_t batch = a.npix / a.HWo;
+    const int64_t gpi = (a.HWo + 7) / 8;
+    const int64_t ntiles = (batch * gpi + kQGran - 1) / kQGran;
+    const int64_t nitems = ntiles * ((a.G + kQWaves - 1) / kQWaves);
+    int64_t wgs = nitems;
+    if (const char* env = std::getenv("ONEXN_PWB_WGS")) {   // workgroup count override (testing)
+        const long v = std::atol(env);
+        if (v >= 1) wgs = std::min<int64_t>(v, nitems);
+    }
+    return launch_grid(pw_bf16<TY>, a, wgs, s, kQThreads);
+}
+
+}  // namespace
+
+bool pw_bf16_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout) {
+    if (xdt != ONEXN_BF16 || layout != ONEXN_NCHW || a.N != 32) return false;
+    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
+    if (a.HWo % 4 != 0 || (reinterpret_cast<uintptr_t>(a.x) & 15) != 0) return false;
+    const int64_t batch = a.npix / a.HWo;
+    if (batch * a.x_img * 2 >= (int64_t(1) << 31)) return false;   // 32-bit buffer offsets
+    if (int64_t(a.t) * 64 >= (int64_t(1) << 31)) return false;
+    (void)ydt;
+    return true;
+}
+
+onexn_status launch_pw_bf16(ConvArgs a, onexn_dtype ydt, hipStream_t s) {
+    if (ydt == ONEXN_BF16) return launch_typed<uint16_t>(a, s);
+    return launch_typed<float>(a, s);
+}
+
+}  // namespace onexn

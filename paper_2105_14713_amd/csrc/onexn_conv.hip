@@ -101,6 +101,7 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
         a.y_pix = n;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
     if (pointwise_applies(a, xdt, ydt, layout)) return launch_pointwise(a, xdt, ydt, s);
     return launch_generic(a, xdt, ydt, s);
 }

@@ -143,17 +143,22 @@ def test_edge_shapes_integer_exact(case):
     np.testing.assert_array_equal(y, ref)
 
 
-@pytest.mark.parametrize("k,N", [(1, 16), (1, 32), (3, 16), (1, 4)])
-def test_out_of_range_channels_are_skipped(k, N):
+@pytest.mark.parametrize("k,N,dt", [(1, 16, "f32"), (1, 32, "f32"), (3, 16, "f32"), (1, 4, "f32"),
+                                    (1, 32, "bf16")])
+def test_out_of_range_channels_are_skipped(k, N, dt):
     """Entries of I outside [0, m) contribute nothing (kept ascending, so the
     rest of the col-group is unaffected); P is clamped to [0, t]."""
-    print(f"skip case k={k} N={N}", flush=True)
-    w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=9)
+    print(f"skip case k={k} N={N} {dt}", flush=True)
+    H = 10 if dt == "bf16" else 9       # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernel
+    w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=H)
+    if dt == "bf16":
+        w, x = w.bfloat16(), x.bfloat16()
     layer = onexn.prepare_layer(w, N, 0.5, False)
     P, I, D = layer.P.cpu(), layer.I.cpu().clone(), layer.D.cpu().clone()
     hi, lo = int(P[1]) - 1, int(P[1])          # last entry of group 0, first of group 1
     I[hi], I[lo] = 1 << 20, -5
-    y = onexn.conv2d_fwd(layer.P, I.cuda(), layer.D, 4 * N, x.cuda(), 1, k // 2)
+    y = onexn.conv2d_fwd(layer.P, I.cuda(), layer.D, 4 * N, x.cuda(), 1, k // 2,
+                         out_dtype=torch.float32)
     # Expected: the same arrays with those two entries' weights zeroed.
     D0 = D.clone()
     D0[hi] = 0
@@ -313,3 +318,34 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
             pytest.skip("resident-tile kernel does not fit this shape")
         ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
         np.testing.assert_array_equal(y, ref)
+
+
+@pytest.mark.parametrize("wgs", ["1", "7", "default"])
+@pytest.mark.parametrize("shape", [
+    dict(m=300, B=3, H=14, W=14),    # 5 channel chunks (ragged last), partial last granule per image
+    dict(m=64, B=2, H=12, W=12),     # one chunk, whole granules, tiles across images
+    dict(m=45, B=1, H=4, W=3),       # fewer pixels than one tile
+    dict(m=700, B=1, H=8, W=6),      # long contraction
+], ids=["m300", "m64", "m45", "m700"])
+def test_pw_bf16_integer_exact(shape, wgs, monkeypatch):
+    """The bf16 pointwise kernel (1x1, N = 32, pixels per image a multiple of
+    4): small integers are exact in bf16 and in fp32 accumulation, so fp32
+    output is bit-exact and bf16 output equals the oracle rounded to bf16.
+    Covers ragged col-groups and a partial last set of 8 col-groups (n = 304),
+    dense to nearly empty col-groups (p = 0, 0.5, 0.97: steps cut short where
+    16 kept channels span more chunks than LDS holds), and workgroup counts
+    that give each workgroup several work items."""
+    if wgs != "default":
+        monkeypatch.setenv("ONEXN_PWB_WGS", wgs)
+    c = shape
+    n = 9 * 32 + 16
+    w, x = workloads.gen_integer_layer(seed=c["m"] + int(c["B"]), cout=n, cin=c["m"], k=1,
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=3, xmax=3)
+    print(f"pw bf16 {c} wgs={wgs}", flush=True)
+    for p in (0.0, 0.5, 0.97):
+        ref, _ = oracle_conv(w, x, 32, p, False, 1, 0)
+        y, _ = gpu_conv(w.bfloat16(), x.bfloat16(), 32, p, False, 1, 0, "nchw", torch.float32)
+        np.testing.assert_array_equal(y, ref)
+        yb, _ = gpu_conv(w.bfloat16(), x.bfloat16(), 32, p, False, 1, 0, "nchw", torch.bfloat16)
+        refb = torch.from_numpy(ref).to(torch.bfloat16).double().numpy()
+        np.testing.assert_array_equal(yb, refb)
