@@ -49,10 +49,13 @@ namespace onexn {
 namespace {
 
 constexpr int kQWaves = 8;                       // compute waves, one col-group each
-constexpr int kQThreads = 64 * (kQWaves + 1);    // + the loader wave
-constexpr int kQKcShift = 6;
+constexpr int kQLoaders = 3;                     // loader waves
+constexpr int kQThreads = 64 * (kQWaves + kQLoaders);
+constexpr int kQKcShift = 5;
 constexpr int kQKc = 1 << kQKcShift;             // input channels per X chunk
-constexpr int kQRing = 3;                        // X chunk buffers
+constexpr int kQRing = 12;                       // X chunk buffers
+constexpr int kQSpan = 4;                        // chunks one k-step may touch
+constexpr int kQInFlight = 2;                    // chunks in flight per loader wave
 constexpr int kQGran = 16;                       // 8-pixel granules per tile
 constexpr int kQCols = 8 * kQGran;               // pixel columns per tile
 constexpr int kQBlocks = kQCols / 32;            // MFMA column blocks
@@ -61,7 +64,7 @@ constexpr int kQBufB = kQKc * kQRowB;            // bytes per chunk buffer
 constexpr int kQCopies = kQBufB / 1024;          // 1 KB copies per chunk
 constexpr int kQZeroOff = kQRing * kQBufB;       // a row of zeros after the ring
 constexpr int kQWin = 16;                        // kept blocks per window (one k-step)
-constexpr int kQWins = 8;                        // windows in a wave's ring
+constexpr int kQWins = 6;                        // windows in a wave's ring
 constexpr int kQRingE = kQWin * kQWins;          // ring entries
 constexpr int kQARowB = 64;                      // bytes of one block's weights (32 bf16)
 constexpr int32_t kQNever = 0x3fffffff;
@@ -156,7 +159,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
     __shared__ __attribute__((aligned(16))) char sA[kQWaves * kQRingE * kQARowB];
     __shared__ __attribute__((aligned(16))) int32_t sI[kQWaves * kQRingE];
     __shared__ int32_t sNeed[kQWaves];
-    __shared__ int32_t sLanded;
+    __shared__ int32_t sFlag[kQRing];   // chunk sequence number that has landed in each buffer
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -172,14 +175,17 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
 
     for (int i = tid; i < kQRowB / 4; i += kQThreads) reinterpret_cast<int32_t*>(sX + kQZeroOff)[i] = 0;
     if (tid < kQWaves) sNeed[tid] = 0;
-    if (tid == 0) sLanded = 0;
+    if (tid < kQRing) sFlag[tid] = -1;
     __syncthreads();
 
     const lds_char* const lx = (const lds_char*)sX;
 
-    if (wave == kQWaves) {
-        // ---- Loader wave: chunk sequence number s = k * nchunks + c (the
-        // workgroup's item k, channel chunk c) goes to buffer s % 3.
+    if (wave >= kQWaves) {
+        // ---- Loader waves.  Chunk sequence number s = k * nchunks + c (the
+        // workgroup's item k, channel chunk c) goes to buffer s % kQRing;
+        // loader wave l copies the chunks with s % kQLoaders == l, up to
+        // kQInFlight at a time, and marks each in sFlag once it has landed.
+        const int32_t ld = wave - kQWaves;
         const v4i32 rX = buffer_rsrc(a.x, int32_t(int64_t(batch) * a.x_img * 2));
         const int h = lane >> 4, q = lane & 15;            // row within a copy (= its rotation), slot
         const int32_t gran = 4 * (((q >> 2) - h) & 3) + (q & 3);   // tile granule held by slot q
@@ -200,7 +206,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             }
             const lds_char* dst = lx + (s % kQRing) * kQBufB;
             const int32_t ch0 = c * kQKc + h;
-#pragma unroll 4
+#pragma unroll
             for (int i = 0; i < kQCopies; ++i) {
                 const int32_t ch = min(ch0 + 4 * i, a.m - 1);   // rows past m copy a real row (never read)
                 copy16_to_lds(rX, dst + i * 1024, pbase + ch * rowb, 0);
@@ -213,25 +219,24 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             for (int w = 0; w < kQWaves; ++w) mn = min(mn, __builtin_amdgcn_readlane(v, w));
             return mn;
         };
-        int32_t issued = 0, landed = 0;
-        while (landed < total_seq) {
-            if (issued < total_seq && issued - landed < 2) {
-                if (min_need() >= issued - (kQRing - 1)) {
-                    issue(issued);
-                    ++issued;
-                    continue;
-                }
-                if (issued == landed) {
-                    __builtin_amdgcn_s_sleep(1);
-                    continue;
-                }
+        int32_t next = ld, oldest = ld, inflight = 0;
+        while (next < total_seq || inflight > 0) {
+            if (next < total_seq && inflight < kQInFlight && min_need() >= next - (kQRing - 1)) {
+                issue(next);
+                next += kQLoaders;
+                ++inflight;
+                continue;
             }
-            if (issued - landed == 2) vm_wait<kQCopies>();
+            if (inflight == 0) {
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            if (inflight == 2) vm_wait<kQCopies>();
             else vm_wait<0>();
-            ++landed;
-            if (lane == 0) lds_store(&sLanded, landed);
+            if (lane == 0) lds_store(&sFlag[oldest % kQRing], oldest);
+            oldest += kQLoaders;
+            --inflight;
         }
-        vm_wait<0>();   // no copy into LDS may outlive the workgroup
         return;
     }
 
@@ -248,7 +253,8 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
     TY* __restrict__ y = static_cast<TY*>(a.y);
 
     f32x16 acc[kQBlocks];
-    int32_t need = 0;
+    int32_t need = 0;      // first chunk this wave may still read (published in sNeed)
+    int32_t landed = 0;    // chunks in [smin, landed) of the current step are known to have landed
     for (int32_t k = 0; k < nloc; ++k) {
         const int32_t item = L + k * a.total;
         const int32_t tile = item / gsets;
@@ -284,9 +290,9 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             // Channel indices for the step at rz: pl (lanes < 16: entry rz +
             // lane), o1 / o2 (entry rz + k1 / rz + k1 + 4).
             auto plan_reads = [&](int32_t rz, int32_t& pl, int32_t& o1, int32_t& o2) {
-                pl = myI[(rz + (lane & 15)) & (kQRingE - 1)];
-                o1 = myI[(rz + k1) & (kQRingE - 1)];
-                o2 = myI[(rz + k1 + 4) & (kQRingE - 1)];
+                pl = myI[(rz + (lane & 15)) % kQRingE];
+                o1 = myI[(rz + k1) % kQRingE];
+                o2 = myI[(rz + k1 + 4) % kQRingE];
             };
             auto plan = [&](int32_t rz, int32_t pl) {
                 QStep st;
@@ -302,12 +308,14 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                     return st;
                 }
                 st.smin = __builtin_amdgcn_readlane(sq, __builtin_ctzll(mv));
-                const uint64_t far = __ballot(okc && sq > st.smin + (kQRing - 1));
+                const uint64_t far = __ballot(okc && sq > st.smin + (kQSpan - 1));
                 st.len = min(avail, far ? int32_t(__builtin_ctzll(far)) : 64);
                 const bool in_step = okc && lane < st.len;
-                st.smax = __ballot(in_step && sq == st.smin + 2) ? st.smin + 2
-                        : __ballot(in_step && sq == st.smin + 1) ? st.smin + 1
-                        : st.smin;
+                int32_t top = st.smin;
+#pragma unroll
+                for (int d = 1; d < kQSpan; ++d)
+                    if (__ballot(in_step && sq == st.smin + d)) top = st.smin + d;
+                st.smax = top;
                 return st;
             };
             // LDS addresses of one lane's entry (k1 + 4 hh) for a step: its A
@@ -324,13 +332,19 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 r.xoff = ok ? ((seq_base + (ch >> kQKcShift)) % kQRing) * kQBufB + row * kQRowB + colb
                             : kQZeroOff + colb;
                 r.rot = ok ? (row & 3) : 0;
-                r.ap = ok ? myA + ((st.rz + e) & (kQRingE - 1)) * kQARowB + colb : zrow + colb;
+                r.ap = ok ? myA + ((st.rz + e) % kQRingE) * kQARowB + colb : zrow + colb;
                 return r;
             };
+            // Waits until the chunks [smin, smax] of a step have landed.  A
+            // buffer's flag only grows (s, s + kQRing, ...), and a buffer
+            // holding a chunk this wave has not released is not refilled, so
+            // flag >= s means chunk s is in place.  Chunks below smin are
+            // never waited for: the wave may have released them unseen.
             auto wait_landed = [&](const QStep& st) {
-                if (st.smax >= 0)
-                    while (__builtin_amdgcn_readfirstlane(lds_load(&sLanded)) <= st.smax)
-                        __builtin_amdgcn_s_sleep(1);
+                for (landed = max(landed, st.smin); landed <= st.smax;) {
+                    if (__builtin_amdgcn_readfirstlane(lds_load(&sFlag[landed % kQRing])) >= landed) ++landed;
+                    else __builtin_amdgcn_s_sleep(1);
+                }
                 fence_compiler();
             };
             auto release = [&](const QStep& st) {
@@ -341,7 +355,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             };
 
             // Prologue: step 0 planned and its fragments read; step 1's indices read.
-            issue_windows(kQWins - 3);
+            issue_windows(kQWins - 1);
             wait_windows(0);
             int32_t pl, o1, o2;
             plan_reads(0, pl, o1, o2);
@@ -376,7 +390,9 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 if (!has_next) nxt.len = 0;
                 if (has_next) {
                     release(nxt);
-                    issue_windows(rz_next / kQWin + kQWins - 1);
+                    // Windows in use: those of steps j+1 and j+2 (at most 3
+                    // from rz_next's); the other slots may be refilled.
+                    issue_windows(rz_next / kQWin + kQWins);
                     wait_landed(nxt);
                 }
                 const int32_t rz2 = rz_next + nxt.len;
