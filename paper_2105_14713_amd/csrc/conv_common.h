@@ -37,6 +37,8 @@ struct ConvArgs {
     int32_t tile_ranges;   // streamed pointwise kernel: pixel-tile ranges per col-group set
     int32_t slices;        // resident-tile pointwise kernel: slices per pixel tile,
     int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder)
+    int32_t kx_rows;       // k x k staged kernel: output rows per tile,
+    int32_t kx_wp, kx_vrwp, kx_cp;   // staged row width, input rows x row width, channel pitch (floats)
 };
 
 // ---------------------------------------------------------------------------
@@ -163,6 +165,8 @@ bool pw_tile_applies(const ConvArgs& a);
 onexn_status launch_pw_tile(ConvArgs a, hipStream_t stream);
 bool pw_bf16_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 onexn_status launch_pw_bf16(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
+bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_kxk(ConvArgs a, hipStream_t stream);
 
 // Launches `kernel` on a 1-D grid of `total` workgroups.
 template <typename K>

@@ -1,0 +1,363 @@
+// k x k (and strided) 1xN-pruned convolution, fp32, N in {16, 32}, NCHW,
+// with the kept channels' input patches and weights staged in LDS.
+//
+// Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
+// (arXiv 2105.14713), Sec. 3.4, Eq. 8.  Col-group g is the contraction
+//     Y_g[N][pixels] = A_g[N][kept_g * k * k] * B_g[kept_g * k * k][pixels]
+// where B_g's row (z, q, r) is input channel I[z] shifted by kernel tap (q, r)
+// under each output pixel (implicit im2col of the kept channels only) and
+// A_g[o][(z, q, r)] = D[z][o][q][r].
+//
+// Work split.  A workgroup computes one (tile, col-group) output block: a tile
+// is R whole output rows (consecutive in batch-major row order, so a tile may
+// span images), at most 256 pixels.  Its four waves split the tile's pixels
+// (NBW MFMA column blocks each) and all of them walk the col-group's kept
+// blocks in chunks of CC blocks.
+//
+// Staging.  For a chunk, the workgroup copies into LDS (buffer loads straight
+// into LDS, double-buffered, one chunk ahead):
+//   * the input rows the tile reads, for each of the chunk's CC channels: the
+//     tile's images' input rows from the first output row's window to the last
+//     one's, stacked ("virtual rows"), each Wp = (Wo - 1) * stride + k wide,
+//     zero where the window leaves the image (padding) -- the zeros come from
+//     out-of-range buffer reads;
+//   * the chunk's CC weight blocks D[z][N][k][k], which are contiguous.
+// Every output pixel's patch at tap (q, r) of staged channel j then sits at
+// LDS float offset j * CP + pofs(pixel) + q * Wp + r.
+//
+// Matrix cores.  N = 32: v_mfma_f32_32x32x2f32; a step is (channel pair, tap):
+// lanes 0-31 take the pair's first channel, lanes 32-63 its second.  N = 16:
+// v_mfma_f32_16x16x4f32; a step is (channel quad, tap), lane group l/16 taking
+// channel l/16 of the quad.  So a lane's A and B addresses differ from step to
+// step by wave-uniform amounts only.  Entries past the col-group's end and
+// channels outside [0, m) stage zero weights and zero inputs.
+#include <cstdlib>
+
+#include "lds_copy.h"
+#include "pw_common.h"
+
+namespace onexn {
+namespace {
+
+constexpr int kKxWaves = 4;
+constexpr int kKxThreads = 64 * kKxWaves;
+constexpr int kKxMaxRem = 9;   // staged positions per lane per channel: (virtual rows x Wp) <= 9 * 256
+
+template <int N, int K, int NBW, int CC>
+__global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
+    typedef PwMfma<N> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int KS = M::KS, COLS = M::COLS, KK = K * K;
+    constexpr int DBUF = CC * N * KK;   // floats of one chunk's weights
+    static_assert(CC % KS == 0 && DBUF % 64 == 0, "chunk shape");
+    extern __shared__ __attribute__((aligned(16))) float smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
+    const int32_t g = L % a.G, tile = L / a.G;
+    int32_t zb, ze;
+    group_range(a, g, zb, ze);
+    const int32_t kept = ze - zb;
+    const int32_t R = a.kx_rows, Wp = a.kx_wp, VRWp = a.kx_vrwp, CP = a.kx_cp;
+    const int32_t XBUF = CC * CP;
+    float* const xs = smem;              // [2][CC][CP]
+    float* const ds = smem + 2 * XBUF;   // [2][CC][N][KK]
+    int32_t* const sI = reinterpret_cast<int32_t*>(ds + 2 * DBUF);   // [3][64]
+
+    // Output rows of the tile, in batch-major order: [rr0, rr1).
+    const int32_t batch = a.npix / a.HWo;
+    const int32_t rr0 = tile * R;
+    const int32_t rr1 = min(rr0 + R, batch * a.Ho);
+    const int32_t b0 = rr0 / a.Ho, blast = (rr1 - 1) / a.Ho;
+    const int32_t oh_first = rr0 - b0 * a.Ho;
+    // Staged input rows of image b (b0 <= b <= blast): its output rows
+    // [lo, hi] read input rows lo * sh - ph .. hi * sh - ph + kh - 1.
+    // A 1x1 kernel reads one input pixel per output pixel, so its staged rows
+    // and columns are the sampled ones only (row (lo + v) * sh - ph, column
+    // col * sw - pw): stride 2 then stages a quarter of the rows' pixels.
+    constexpr bool kSub = K == 1;
+    auto seg_lo = [&](int32_t b) { return b == b0 ? oh_first : 0; };
+    auto seg_rows = [&](int32_t b) {
+        const int32_t hi = b == blast ? rr1 - 1 - b * a.Ho : a.Ho - 1;
+        return kSub ? hi - seg_lo(b) + 1 : (hi - seg_lo(b)) * a.sh + K;
+    };
+
+    // Byte offset in x of each staged position this lane copies (channel 0),
+    // or kBufferOutOfRange where the window leaves the image.
+    uint32_t spk[kKxMaxRem];
+#pragma unroll
+    for (int k = 0; k < kKxMaxRem; ++k) {
+        const int32_t rem = wave * 64 + lane + k * kKxThreads;
+        uint32_t sp = kBufferOutOfRange;
+        if (rem < VRWp) {
+            int32_t v = rem / Wp;
+            const int32_t col = rem - v * Wp;
+            int32_t b = b0;
+            for (; b <= blast; ++b) {
+                const int32_t nv = seg_rows(b);
+                if (v < nv) break;
+                v -= nv;
+            }
+            const int32_t ih = kSub ? (seg_lo(b) + v) * a.sh - a.ph : seg_lo(b) * a.sh - a.ph + v;
+            const int32_t iw = kSub ? col * a.sw - a.pw : col - a.pw;
+            if (b <= blast && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                sp = uint32_t((int64_t(b) * a.x_img + int64_t(ih) * a.W + iw) * 4);
+        }
+        spk[k] = sp;
+    }
+
+    // This lane's output pixel in each of its column blocks: LDS offset of its
+    // patch within a staged channel, and its y offset (-1: not a pixel).
+    int32_t pofs[NBW];
+    int64_t ybase[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int32_t i = (wave * NBW + nb) * COLS + lane % COLS;
+        const int32_t r = i / a.Wo, ow = i - r * a.Wo;
+        const int32_t rr = rr0 + r;
+        pofs[nb] = 0;
+        ybase[nb] = -1;
+        if (r < R && rr < rr1) {
+            const int32_t b = rr / a.Ho, oh = rr - b * a.Ho;
+            int32_t vb = 0;
+            for (int32_t bb = b0; bb < b; ++bb) vb += seg_rows(bb);
+            pofs[nb] = kSub ? (vb + oh - seg_lo(b)) * Wp + ow : (vb + (oh - seg_lo(b)) * a.sh) * Wp + ow * a.sw;
+            ybase[nb] = int64_t(b) * a.y_img + int64_t(oh) * a.Wo + ow;
+        }
+    }
+
+    const v4i32 rX = buffer_rsrc(a.x, int32_t(int64_t(batch) * a.x_img * 4));
+    const v4i32 rD = buffer_rsrc(a.D, int32_t(int64_t(ze) * N * KK * 4));
+    const v4i32 rI = buffer_rsrc(a.I, int32_t(int64_t(ze) * 4));
+    const int32_t nchunks = (kept + CC - 1) / CC;
+
+    // The channel indices of chunk c sit in LDS ring slot c % 3 (64 entries,
+    // copied by wave 0 two chunks ahead, like the other operands).
+    auto copy_channels = [&](int32_t c) {
+        if (wave == 0)
+            copy4_to_lds(rI, (const lds_char*)(sI + (c % 3) * 64), (zb + c * CC + lane) * 4, 0);
+    };
+    // Stages chunk c: its weight blocks and its channels' input rows.
+    auto stage = [&](int32_t c, int buf) {
+        const lds_char* dd = (const lds_char*)(ds + buf * DBUF);
+        const int32_t d0 = (zb + c * CC) * (N * KK * 4);
+        for (int32_t e0 = wave * 64; e0 < DBUF; e0 += kKxThreads)
+            copy4_to_lds(rD, dd + e0 * 4, d0 + (e0 + lane) * 4, 0);
+        // Lane j < CC: block j's channel, or -1 past the col-group's end.
+        const int32_t chv = (lane < CC && zb + c * CC + lane < ze) ? sI[(c % 3) * 64 + lane] : -1;
+        const lds_char* xd = (const lds_char*)(xs + buf * XBUF);
+#pragma unroll
+        for (int j = 0; j < CC; ++j) {
+            const int32_t ch = __builtin_amdgcn_readlane(chv, j);
+            const uint32_t choff = (ch >= 0 && ch < a.m) ? uint32_t(ch) * uint32_t(a.x_c) * 4u : kBufferOutOfRange;
+#pragma unroll
+            for (int k = 0; k < kKxMaxRem; ++k) {
+                const int32_t rem0 = wave * 64 + k * kKxThreads;
+                if (rem0 < VRWp)
+                    copy4_to_lds(rX, xd + (j * CP + rem0) * 4, int32_t(min(spk[k] + choff, kBufferOutOfRange)), 0);
+            }
+        }
+    };
+
+    acc_t acc[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) acc[nb][r] = 0.f;
+
+    // Lane roles: row / pixel column o = lane % COLS, staged channel kq of a
+    // step.  A chunk is always computed whole: its slots past the col-group's
+    // end hold zero weights and zero inputs.
+    const int o = lane % COLS, kq = lane / COLS;
+    auto compute = [&](int buf) {
+        const float* xb = xs + buf * XBUF + kq * CP;
+        const float* db = ds + buf * DBUF + (kq * N + o) * KK;
+        constexpr int S = (CC / KS) * KK;   // MFMA steps of a chunk: (slot group, tap)
+        auto read = [&](int st, float& av, float (&bv)[NBW]) {
+            const int jg = st / KK, tap = st % KK;
+            const int q = tap / K, r = tap % K;
+            av = db[jg * KS * N * KK + tap];
+            const float* xj = xb + jg * KS * CP + q * Wp + r;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) bv[nb] = xj[pofs[nb]];
+        };
+        // Software pipeline: step st + PD's operands are read from LDS while
+        // step st's MFMAs run; the scheduling groups put one MFMA between
+        // each pair of reads.
+        constexpr int PD = 2;
+        float av[PD + 1], bv[PD + 1][NBW];
+#pragma unroll
+        for (int st = 0; st < PD && st < S; ++st) read(st, av[st], bv[st]);
+#pragma unroll
+        for (int st = 0; st < S; ++st) {
+            const int cur = st % (PD + 1);
+            if (st + PD < S) read(st + PD, av[(st + PD) % (PD + 1)], bv[(st + PD) % (PD + 1)]);
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) acc[nb] = M::step(av[cur], bv[cur][nb], acc[nb]);
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // an LDS read,
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // an MFMA
+            }
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);       // address arithmetic
+        }
+    };
+
+    // Chunk c + 1 is staged while chunk c is multiplied; one barrier per chunk
+    // hands the buffers over.
+    if (nchunks > 0) {
+        copy_channels(0);
+        copy_channels(1);
+        vm_wait<0>();
+        __syncthreads();
+        stage(0, 0);
+        copy_channels(2);
+    }
+    vm_wait<0>();
+    __syncthreads();
+    for (int32_t c = 0; c < nchunks; ++c) {
+        if (c + 1 < nchunks) {
+            stage(c + 1, (c + 1) & 1);
+            copy_channels(c + 3);
+        }
+        compute(c & 1);
+        vm_wait<0>();
+        __syncthreads();
+    }
+
+    // Store: MFMA (row, col) of column block nb -> output channel g*N + row.
+    float* __restrict__ y = static_cast<float*>(a.y);
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        if (ybase[nb] < 0) continue;
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) {
+            const int32_t oc = g * N + M::row(lane, r);
+            if (oc < a.n) y[ybase[nb] + int64_t(oc) * a.y_c] = acc[nb][r];
+        }
+    }
+}
+
+struct KxShape {
+    int32_t rows = 0, wp = 0, vrwp = 0, cp = 0;
+    int tp = 0;   // pixel capacity of the tile (4 waves x NBW x MFMA columns)
+};
+
+// Largest number of staged input rows any tile of `rows` output rows needs.
+// A tile's row structure depends only on where it starts within an image, so
+// the first min(tiles, Ho) tiles cover every case.
+int32_t max_virtual_rows(const ConvArgs& a, int32_t rows) {
+    const int64_t nrows = int64_t(a.npix / a.HWo) * a.Ho;
+    const int64_t ntiles = (nrows + rows - 1) / rows;
+    int32_t best = 0;
+    for (int64_t t = 0; t < std::min<int64_t>(ntiles, a.Ho); ++t) {
+        const int64_t r0 = t * rows, r1 = std::min<int64_t>(r0 + rows, nrows);
+        int32_t v = 0;
+        for (int64_t b = r0 / a.Ho; b <= (r1 - 1) / a.Ho; ++b) {
+            const int64_t lo = b == r0 / a.Ho ? r0 - b * a.Ho : 0;
+            const int64_t hi = b == (r1 - 1) / a.Ho ? r1 - 1 - b * a.Ho : a.Ho - 1;
+            v += int32_t(a.kh == 1 ? hi - lo + 1 : (hi - lo) * a.sh + a.kh);
+        }
+        best = std::max(best, v);
+    }
+    return best;
+}
+
+template <int N>
+constexpr int kx_cols() { return N == 32 ? 32 : 16; }
+
+// Dynamic LDS of a launch: two chunk buffers of inputs and weights, and the
+// ring of channel indices.
+int64_t kx_lds_bytes(int cc, int cp, int N, int KK) {
+    return 2 * 4 * (int64_t(cc) * cp + int64_t(cc) * N * KK) + 3 * 64 * 4;
+}
+
+// Tile and LDS shape for a pixel capacity tp, or rows == 0 when it does not fit.
+KxShape kx_shape(const ConvArgs& a, int tp, int cc) {
+    KxShape s;
+    s.tp = tp;
+    if (a.Wo > tp) return s;
+    s.rows = tp / a.Wo;
+    s.wp = a.kh == 1 ? a.Wo : (a.Wo - 1) * a.sw + a.kw;   // 1x1: sampled columns only
+    s.vrwp = max_virtual_rows(a, s.rows) * s.wp;
+    const int cols = a.N == 32 ? 32 : 16;
+    s.cp = (s.vrwp + 63) / 64 * 64 + cols;   // whole 64-float copies; halves of a step land on other banks
+    const int64_t lds = kx_lds_bytes(cc, s.cp, a.N, a.KK);
+    if (s.vrwp > kKxMaxRem * kKxThreads || lds > 64 * 1024) s.rows = 0;
+    return s;
+}
+
+int kx_cc(int N, int k) {
+    if (k == 7) return N == 32 ? 2 : 4;
+    if (k == 1) return 16;
+    return 8;
+}
+
+template <int N, int K, int NBW>
+onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
+    constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : (K == 1 ? 16 : 8);
+    a.kx_rows = s.rows;
+    a.kx_wp = s.wp;
+    a.kx_vrwp = s.vrwp;
+    a.kx_cp = s.cp;
+    const int64_t nrows = int64_t(a.npix / a.HWo) * a.Ho;
+    const int64_t total = (nrows + s.rows - 1) / s.rows * a.G;
+    if (total < 1 || total > INT32_MAX / kKxThreads)
+        return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: grid of %lld workgroups is out of range",
+                    (long long)total);
+    a.total = int32_t(total);
+    const size_t lds = size_t(kx_lds_bytes(CC, s.cp, N, K * K));
+    hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess)
+        return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(err));
+    return ONEXN_OK;
+}
+
+// Picks the tile size: 256 pixels when that still gives the GPU a few
+// workgroups per compute unit, else 128.
+template <int N, int K>
+onexn_status launch_k(ConvArgs a, hipStream_t stream) {
+    constexpr int COLS = kx_cols<N>();
+    constexpr int NB_BIG = 256 / (4 * COLS), NB_SMALL = 128 / (4 * COLS);
+    const int cc = kx_cc(N, K);
+    const KxShape big = kx_shape(a, 256, cc), small = kx_shape(a, 128, cc);
+    const int64_t nrows = int64_t(a.npix / a.HWo) * a.Ho;
+    const int64_t want = 3 * int64_t(device_cu_count());
+    bool big_ok = big.rows > 0 && (nrows + big.rows - 1) / big.rows * a.G >= want;
+    if (const char* env = std::getenv("ONEXN_KXK_TP")) {   // tile capacity override (testing)
+        const int v = std::atoi(env);
+        if (v == 256 && big.rows > 0) big_ok = true;
+        if (v == 128 && small.rows > 0) big_ok = false;
+    }
+    if (big_ok || (big.rows > 0 && small.rows == 0)) return launch_nbw<N, K, NB_BIG>(a, big, stream);
+    return launch_nbw<N, K, NB_SMALL>(a, small, stream);
+}
+
+}  // namespace
+
+bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout) {
+    if (xdt != ONEXN_F32 || ydt != ONEXN_F32 || layout != ONEXN_NCHW) return false;
+    if (a.N != 16 && a.N != 32) return false;
+    if (a.kh != a.kw || (a.kh != 1 && a.kh != 3 && a.kh != 7)) return false;
+    const int64_t batch = a.npix / a.HWo;
+    if (batch * a.x_img * 4 >= (int64_t(1) << 31)) return false;        // 32-bit buffer offsets
+    if (int64_t(a.t) * a.N * a.KK * 4 >= (int64_t(1) << 31)) return false;
+    const int cc = kx_cc(a.N, a.kh);
+    return kx_shape(a, 256, cc).rows > 0 || kx_shape(a, 128, cc).rows > 0;
+}
+
+onexn_status launch_kxk(ConvArgs a, hipStream_t stream) {
+    if (a.N == 32) {
+        if (a.kh == 1) return launch_k<32, 1>(a, stream);
+        if (a.kh == 3) return launch_k<32, 3>(a, stream);
+        return launch_k<32, 7>(a, stream);
+    }
+    if (a.kh == 1) return launch_k<16, 1>(a, stream);
+    if (a.kh == 3) return launch_k<16, 3>(a, stream);
+    return launch_k<16, 7>(a, stream);
+}
+
+}  // namespace onexn

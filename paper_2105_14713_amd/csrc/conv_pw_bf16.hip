@@ -43,6 +43,7 @@
 // B, so they add exactly nothing.
 #include <cstdlib>
 
+#include "lds_copy.h"
 #include "pw_common.h"
 
 namespace onexn {
@@ -68,22 +69,9 @@ constexpr int kQWins = 6;                        // windows in a wave's ring
 constexpr int kQRingE = kQWin * kQWins;          // ring entries
 constexpr int kQARowB = 64;                      // bytes of one block's weights (32 bf16)
 constexpr int32_t kQNever = 0x3fffffff;
-constexpr int32_t kQBufferFlags = 0x00020000;    // buffer resource word 3: 32-bit raw data
-
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
-typedef int v4i32 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-
-__device__ __forceinline__ int32_t lds_load(const int32_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ void lds_store(int32_t* p, int32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-// Compiler-only barrier: no memory access moves across it.
-__device__ __forceinline__ void fence_compiler() { asm volatile("" ::: "memory"); }
 
 __device__ __forceinline__ v4i16 tr_read(const lds_char* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p);
@@ -92,46 +80,6 @@ __device__ __forceinline__ v4i16 tr_read(const lds_char* p) {
 __device__ __forceinline__ bf16x8 join(v4i16 lo, v4i16 hi) {
     const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     return __builtin_bit_cast(bf16x8, v);
-}
-
-// Raw buffer resource over [p, p + bytes): reads past the end return zeros.
-__device__ __forceinline__ v4i32 buffer_rsrc(const void* p, int32_t bytes) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    v4i32 r;
-    r.x = __builtin_amdgcn_readfirstlane(int32_t(uint32_t(v)));
-    r.y = __builtin_amdgcn_readfirstlane(int32_t(uint32_t(v >> 32) & 0xffff));
-    r.z = __builtin_amdgcn_readfirstlane(bytes);
-    r.w = kQBufferFlags;
-    return r;
-}
-
-// (m0 is named as clobbered for the reader; the compiler keeps nothing in it here.)
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-// Copies from a buffer straight into LDS: lane i's 16 (or 4) bytes at byte
-// offset voff + soff land at LDS address dst + 16 i (4 i).  Written as inline
-// assembly so that the compiler, which cannot tell which LDS bytes such a copy
-// writes, does not make every later LDS read wait for all outstanding copies;
-// the kernel orders them itself with the waits below.
-__device__ __forceinline__ void copy16_to_lds(v4i32 rs, const lds_char* dst, int32_t voff, int32_t soff) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(dst)));
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 :: "s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
-}
-__device__ __forceinline__ void copy4_to_lds(v4i32 rs, const lds_char* dst, int32_t voff, int32_t soff) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(dst)));
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
-                 :: "s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
-}
-
-#pragma clang diagnostic pop
-
-// Waits until at most N vector-memory instructions of this wave are
-// outstanding; also a compiler barrier for memory accesses.
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
 // Waits until at most n (even) copies are outstanding; n is wave-uniform.
@@ -213,7 +161,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             }
         };
         auto min_need = [&]() {
-            const int32_t v = lane < kQWaves ? lds_load(&sNeed[lane]) : kQNever;
+            const int32_t v = lane < kQWaves ? lds_flag_load(&sNeed[lane]) : kQNever;
             int32_t mn = kQNever;
 #pragma unroll
             for (int w = 0; w < kQWaves; ++w) mn = min(mn, __builtin_amdgcn_readlane(v, w));
@@ -233,7 +181,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             }
             if (inflight == 2) vm_wait<kQCopies>();
             else vm_wait<0>();
-            if (lane == 0) lds_store(&sFlag[oldest % kQRing], oldest);
+            if (lane == 0) lds_flag_store(&sFlag[oldest % kQRing], oldest);
             oldest += kQLoaders;
             --inflight;
         }
@@ -277,9 +225,9 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 upto = min(upto, nwin);
                 for (; wi < upto; ++wi) {
                     const int32_t slot = wi % kQWins;
-                    copy16_to_lds(rA, myA + slot * (kQWin * kQARowB), lane * 16, (zb + wi * kQWin) * kQARowB);
+                    copy16_to_lds(rA, myA + slot * (kQWin * kQARowB), lane * 16 + (zb + wi * kQWin) * kQARowB, 0);
                     if (lane < kQWin)
-                        copy4_to_lds(rI, (const lds_char*)myI + slot * (kQWin * 4), lane * 4, (zb + wi * kQWin) * 4);
+                        copy4_to_lds(rI, (const lds_char*)myI + slot * (kQWin * 4), lane * 4 + (zb + wi * kQWin) * 4, 0);
                 }
             };
             // Waits until the windows holding entries rz .. rz + 15 have landed.
@@ -342,7 +290,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             // never waited for: the wave may have released them unseen.
             auto wait_landed = [&](const QStep& st) {
                 for (landed = max(landed, st.smin); landed <= st.smax;) {
-                    if (__builtin_amdgcn_readfirstlane(lds_load(&sFlag[landed % kQRing])) >= landed) ++landed;
+                    if (__builtin_amdgcn_readfirstlane(lds_flag_load(&sFlag[landed % kQRing])) >= landed) ++landed;
                     else __builtin_amdgcn_s_sleep(1);
                 }
                 fence_compiler();
@@ -350,7 +298,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             auto release = [&](const QStep& st) {
                 if (st.smin > need) {
                     need = st.smin;
-                    if (lane == 0) lds_store(&sNeed[w], need);
+                    if (lane == 0) lds_flag_store(&sNeed[w], need);
                 }
             };
 
@@ -420,7 +368,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
         // Past this item's chunks.
         if (seq_base + nchunks > need) {
             need = seq_base + nchunks;
-            if (lane == 0) lds_store(&sNeed[w], need);
+            if (lane == 0) lds_flag_store(&sNeed[w], need);
         }
 
         // Store: MFMA (row, col) of block e -> output channel g*32 + row, tile column 32e + col.
@@ -441,7 +389,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             }
         }
     }
-    if (lane == 0) lds_store(&sNeed[w], kQNever);
+    if (lane == 0) lds_flag_store(&sNeed[w], kQNever);
 }
 
 template <typename TY>

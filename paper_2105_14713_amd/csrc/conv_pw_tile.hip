@@ -248,9 +248,10 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
         int32_t s, len, ze, base, g, slice;
         bool last, valid;
     };
-    // I and D are read through buffer resources: a scalar base per block, a
-    // constant lane offset and an immediate per step, so a block's loads cost
-    // no vector instructions; reads past the arrays return 0.  A block always
+    // I and D are read through buffer resources with the whole offset (block
+    // start plus lane position) in the vector offset, which the hardware
+    // range-checks (the scalar offset is not checked): reads past the arrays
+    // return 0 and never leave them.  A block always
     // loads BLK entries: entries past len belong to the next col-group (or
     // are zeros past t) and meet the zero row of X.
     const __amdgpu_buffer_rsrc_t rI =
@@ -260,12 +261,12 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     const int lg = lane / N, lo = lane % N;
     const int32_t lane_i = (lane % BLK) * 4, lane_d = lane * 4;
     auto load_ch = [&](int32_t& ch, const Desc& d) {
-        ch = __builtin_amdgcn_raw_buffer_load_b32(rI, lane_i, d.s * 4, 0);
+        ch = __builtin_amdgcn_raw_buffer_load_b32(rI, lane_i + d.s * 4, 0, 0);
     };
     auto load_w = [&](float (&av)[STEPS], const Desc& d) {
 #pragma unroll
         for (int ks = 0; ks < STEPS; ++ks)
-            av[ks] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, lane_d + ks * KS * N * 4, d.s * N * 4, 0));
+            av[ks] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, lane_d + ks * KS * N * 4 + d.s * N * 4, 0, 0));
     };
     // Row offsets of a block, one per step for this lane's group: lane i of
     // the block names entry i's X row (lanes i >= len and channels outside

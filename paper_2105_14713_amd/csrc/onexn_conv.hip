@@ -2,6 +2,8 @@
 // kernel family (pointwise LDS-shared kernels for 1x1 stride-1 NCHW layers
 // where they apply, the generic gather kernels otherwise).
 #include <atomic>
+#include <cstdlib>
+#include <cstring>
 
 #include "conv_common.h"
 
@@ -19,6 +21,14 @@ int device_cu_count() {
     cache[dev].store(v, std::memory_order_relaxed);
     return v;
 }
+
+// ONEXN_KERNEL=generic sends every layer the specialised kernels would take
+// to the generic gather kernels instead (for comparing the two).
+bool env_is(const char* name, const char* value) {
+    const char* env = std::getenv(name);
+    return env && std::strcmp(env, value) == 0;
+}
+bool generic_forced() { return env_is("ONEXN_KERNEL", "generic"); }
 
 }  // namespace onexn
 
@@ -102,6 +112,8 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
-    if (pointwise_applies(a, xdt, ydt, layout)) return launch_pointwise(a, xdt, ydt, s);
+    if (pointwise_applies(a, xdt, ydt, layout) && !env_is("ONEXN_PW_KERNEL", "kxk"))
+        return launch_pointwise(a, xdt, ydt, s);
+    if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     return launch_generic(a, xdt, ydt, s);
 }

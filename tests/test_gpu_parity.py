@@ -349,3 +349,69 @@ def test_pw_bf16_integer_exact(shape, wgs, monkeypatch):
         yb, _ = gpu_conv(w.bfloat16(), x.bfloat16(), 32, p, False, 1, 0, "nchw", torch.bfloat16)
         refb = torch.from_numpy(ref).to(torch.bfloat16).double().numpy()
         np.testing.assert_array_equal(yb, refb)
+
+
+@pytest.mark.parametrize("tp", ["128", "256"])
+@pytest.mark.parametrize("case", [
+    dict(k=3, s=1, pd=1, B=2, H=56, W=56, m=20, N=32),   # 4 whole rows per tile
+    dict(k=3, s=1, pd=1, B=5, H=14, W=14, m=37, N=32),   # tiles span images
+    dict(k=3, s=2, pd=1, B=3, H=28, W=28, m=19, N=32),   # stride 2: rows straddle images
+    dict(k=3, s=1, pd=1, B=9, H=7, W=7, m=70, N=16),     # many images per tile
+    dict(k=3, s=1, pd=0, B=2, H=11, W=13, m=9, N=16),    # no padding, non-square
+    dict(k=1, s=2, pd=0, B=3, H=28, W=28, m=45, N=32),   # strided 1x1 (downsample)
+    dict(k=1, s=2, pd=0, B=2, H=15, W=9, m=40, N=16),
+    dict(k=7, s=2, pd=3, B=2, H=40, W=40, m=3, N=32),    # stem-like: 3 channels
+    dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=16),
+], ids=lambda c: f"k{c['k']}s{c['s']}p{c['pd']}_B{c['B']}_{c['H']}x{c['W']}_m{c['m']}_N{c['N']}")
+def test_kxk_integer_exact(case, tp, monkeypatch):
+    """The LDS-staged k x k kernel at both tile sizes: tiles of whole output
+    rows that span images, padding and stride, ragged last col-group, and p
+    from dense to nearly empty (chunks with fewer kept blocks than a step)."""
+    monkeypatch.setenv("ONEXN_KXK_TP", tp)
+    c = case
+    n = 2 * c["N"] + c["N"] // 2
+    w, x = workloads.gen_integer_layer(seed=c["m"] * 7 + c["k"], cout=n, cin=c["m"], k=c["k"],
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=2, xmax=3)
+    print(f"kxk {c} tp={tp}", flush=True)
+    for p in (0.0, 0.5, 0.9):
+        y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        np.testing.assert_array_equal(y, ref)
+
+
+def test_kxk_matches_generic_on_random_fp32(monkeypatch):
+    """Random-valued fp32 3x3 layer: the staged kernel and the oracle agree to
+    1e-5 of max |y| over a contraction of 288 * 9 entries."""
+    gen = torch.Generator().manual_seed(11)
+    w = workloads.gen_weight(gen, 96, 288, 3)
+    x = workloads.gen_activation(gen, (3, 288, 14, 14))
+    y, _ = gpu_conv(w, x, 32, 0.5, True, 1, 1)
+    ref, _ = oracle_conv(w, x, 32, 0.5, True, 1, 1)
+    assert rel_err(y, ref) <= 1e-5
+
+
+@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma"])
+def test_reads_stay_inside_I_and_D(kind, monkeypatch):
+    """I and D are views at the start of larger buffers whose tails hold a
+    valid channel index (0) and NaN weights: a kernel that used any entry past
+    t would put NaN into the output."""
+    k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
+                      "stream": (1, 32, 300, torch.float32, 12), "bf16": (1, 32, 96, torch.bfloat16, 12),
+                      "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12)}[kind]
+    if kind in ("tile", "stream"):
+        monkeypatch.setenv("ONEXN_PW_KERNEL", kind)
+    n = 3 * N + N // 2
+    w, x = workloads.gen_integer_layer(seed=7, cout=n, cin=m, k=k, batch=2, H=H, wmax=2, xmax=2)
+    w, x = w.to(dt), x.to(dt)
+    layer = onexn.prepare_layer(w, N, 0.5, False)
+    t = layer.t
+    extra = 4096
+    I_big = torch.zeros(t + extra, dtype=torch.int32, device="cuda")
+    I_big[:t] = layer.I
+    D_big = torch.full((t + extra, N, k, k), float("nan"), dtype=dt, device="cuda")
+    D_big[:t] = layer.D
+    pd = k // 2
+    y = onexn.conv2d_fwd(layer.P, I_big[:t], D_big[:t], n, x.cuda(), 1, pd, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref, _ = oracle_conv(w.float(), x.float(), N, 0.5, False, 1, pd)
+    np.testing.assert_array_equal(y.double().cpu().numpy(), ref)
