@@ -1,4 +1,5 @@
-// k x k (and strided) 1xN-pruned convolution, fp32, N in {16, 32}, NCHW,
+// 3x3 and 7x7 (any stride and padding) 1xN-pruned convolution, fp32,
+// N in {16, 32}, NCHW,
 // with the kept channels' input patches and weights staged in LDS.
 //
 // Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
@@ -73,14 +74,10 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
     const int32_t oh_first = rr0 - b0 * a.Ho;
     // Staged input rows of image b (b0 <= b <= blast): its output rows
     // [lo, hi] read input rows lo * sh - ph .. hi * sh - ph + kh - 1.
-    // A 1x1 kernel reads one input pixel per output pixel, so its staged rows
-    // and columns are the sampled ones only (row (lo + v) * sh - ph, column
-    // col * sw - pw): stride 2 then stages a quarter of the rows' pixels.
-    constexpr bool kSub = K == 1;
     auto seg_lo = [&](int32_t b) { return b == b0 ? oh_first : 0; };
     auto seg_rows = [&](int32_t b) {
         const int32_t hi = b == blast ? rr1 - 1 - b * a.Ho : a.Ho - 1;
-        return kSub ? hi - seg_lo(b) + 1 : (hi - seg_lo(b)) * a.sh + K;
+        return (hi - seg_lo(b)) * a.sh + K;
     };
 
     // Byte offset in x of each staged position this lane copies (channel 0),
@@ -99,8 +96,7 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
                 if (v < nv) break;
                 v -= nv;
             }
-            const int32_t ih = kSub ? (seg_lo(b) + v) * a.sh - a.ph : seg_lo(b) * a.sh - a.ph + v;
-            const int32_t iw = kSub ? col * a.sw - a.pw : col - a.pw;
+            const int32_t ih = seg_lo(b) * a.sh - a.ph + v, iw = col - a.pw;
             if (b <= blast && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
                 sp = uint32_t((int64_t(b) * a.x_img + int64_t(ih) * a.W + iw) * 4);
         }
@@ -122,7 +118,7 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
             const int32_t b = rr / a.Ho, oh = rr - b * a.Ho;
             int32_t vb = 0;
             for (int32_t bb = b0; bb < b; ++bb) vb += seg_rows(bb);
-            pofs[nb] = kSub ? (vb + oh - seg_lo(b)) * Wp + ow : (vb + (oh - seg_lo(b)) * a.sh) * Wp + ow * a.sw;
+            pofs[nb] = (vb + (oh - seg_lo(b)) * a.sh) * Wp + ow * a.sw;
             ybase[nb] = int64_t(b) * a.y_img + int64_t(oh) * a.Wo + ow;
         }
     }
@@ -258,7 +254,7 @@ int32_t max_virtual_rows(const ConvArgs& a, int32_t rows) {
         for (int64_t b = r0 / a.Ho; b <= (r1 - 1) / a.Ho; ++b) {
             const int64_t lo = b == r0 / a.Ho ? r0 - b * a.Ho : 0;
             const int64_t hi = b == (r1 - 1) / a.Ho ? r1 - 1 - b * a.Ho : a.Ho - 1;
-            v += int32_t(a.kh == 1 ? hi - lo + 1 : (hi - lo) * a.sh + a.kh);
+            v += int32_t((hi - lo) * a.sh + a.kh);
         }
         best = std::max(best, v);
     }
@@ -280,7 +276,7 @@ KxShape kx_shape(const ConvArgs& a, int tp, int cc) {
     s.tp = tp;
     if (a.Wo > tp) return s;
     s.rows = tp / a.Wo;
-    s.wp = a.kh == 1 ? a.Wo : (a.Wo - 1) * a.sw + a.kw;   // 1x1: sampled columns only
+    s.wp = (a.Wo - 1) * a.sw + a.kw;
     s.vrwp = max_virtual_rows(a, s.rows) * s.wp;
     const int cols = a.N == 32 ? 32 : 16;
     s.cp = (s.vrwp + 63) / 64 * 64 + cols;   // whole 64-float copies; halves of a step land on other banks
@@ -289,15 +285,11 @@ KxShape kx_shape(const ConvArgs& a, int tp, int cc) {
     return s;
 }
 
-int kx_cc(int N, int k) {
-    if (k == 7) return N == 32 ? 2 : 4;
-    if (k == 1) return 16;
-    return 8;
-}
+int kx_cc(int N, int k) { return k == 7 ? (N == 32 ? 2 : 4) : 8; }
 
 template <int N, int K, int NBW>
 onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
-    constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : (K == 1 ? 16 : 8);
+    constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : 8;
     a.kx_rows = s.rows;
     a.kx_wp = s.wp;
     a.kx_vrwp = s.vrwp;
@@ -341,7 +333,9 @@ onexn_status launch_k(ConvArgs a, hipStream_t stream) {
 bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout) {
     if (xdt != ONEXN_F32 || ydt != ONEXN_F32 || layout != ONEXN_NCHW) return false;
     if (a.N != 16 && a.N != 32) return false;
-    if (a.kh != a.kw || (a.kh != 1 && a.kh != 3 && a.kh != 7)) return false;
+    // 1x1 layers stay on the pointwise and generic kernels, which measured
+    // faster for them (a staged 1x1 chunk carries too little work).
+    if (a.kh != a.kw || (a.kh != 3 && a.kh != 7)) return false;
     const int64_t batch = a.npix / a.HWo;
     if (batch * a.x_img * 4 >= (int64_t(1) << 31)) return false;        // 32-bit buffer offsets
     if (int64_t(a.t) * a.N * a.KK * 4 >= (int64_t(1) << 31)) return false;
@@ -351,11 +345,9 @@ bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layo
 
 onexn_status launch_kxk(ConvArgs a, hipStream_t stream) {
     if (a.N == 32) {
-        if (a.kh == 1) return launch_k<32, 1>(a, stream);
         if (a.kh == 3) return launch_k<32, 3>(a, stream);
         return launch_k<32, 7>(a, stream);
     }
-    if (a.kh == 1) return launch_k<16, 1>(a, stream);
     if (a.kh == 3) return launch_k<16, 3>(a, stream);
     return launch_k<16, 7>(a, stream);
 }

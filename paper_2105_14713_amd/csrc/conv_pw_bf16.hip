@@ -23,20 +23,23 @@
 // 8 pixels; a granule lies in one image (the last granule of an image may be
 // partial), so that each granule of a channel is one 16-byte copy.
 //
-// Input staging.  The workgroup's ninth wave copies X into LDS in chunks of 64
-// channels x 128 columns (16 KB) with buffer loads straight into LDS, into a
-// ring of 3 chunk buffers, as far ahead as the ring allows.  Rows are stored
-// with their four 64-byte column blocks rotated by (row mod 4), so that the 8
-// rows one transposed read touches spread over the LDS banks.  LDS counters,
-// not barriers, order the two sides: `landed` counts chunks in LDS, each
-// compute wave's `need` is the first chunk it may still read; a buffer is
-// refilled once every wave's `need` has passed the chunk in it.
+// Input staging.  Three loader waves copy X into LDS in chunks of 32
+// channels x 128 columns with buffer loads straight into LDS (16 bytes per
+// lane, four 256-byte rows per copy), into a ring of 8 chunk buffers, as far
+// ahead as the ring allows.  Each group of 4 rows is followed by 64 bytes of
+// padding, so the 8 rows one transposed read touches spread over the LDS
+// banks while a row's four 64-byte column blocks stay at fixed offsets
+// (immediates of the reads).
+// LDS flags, not barriers, order the two sides: each buffer's flag names the
+// chunk that has landed in it, each compute wave's `need` is the first chunk
+// it may still read; a buffer is refilled once every wave's `need` has passed
+// the chunk in it.
 //
 // Kept blocks.  A compute wave walks its col-group's kept blocks in steps of
 // up to 16 (one MFMA k-step): a step takes the next 16 blocks unless their
-// channels span more than the 3 chunks the ring holds, in which case it stops
-// short.  The blocks' weights (16 x 64 bytes) and channel indices are copied
+// channels span more than 4 chunks, in which case it stops short.  The blocks' weights (16 x 64 bytes) and channel indices are copied
 // into a per-wave LDS ring in windows of 16 blocks, up to 5 windows ahead.
+// Ring sizes are powers of two so that every slot index is a mask.
 // Steps are software-pipelined: while step j's four MFMAs run, the wave reads
 // step j+1's A and B fragments and step j+2's channel indices.  Entries past
 // a step's end, and channels outside [0, m), read a zero row for both A and
@@ -54,18 +57,19 @@ constexpr int kQLoaders = 3;                     // loader waves
 constexpr int kQThreads = 64 * (kQWaves + kQLoaders);
 constexpr int kQKcShift = 5;
 constexpr int kQKc = 1 << kQKcShift;             // input channels per X chunk
-constexpr int kQRing = 12;                       // X chunk buffers
+constexpr int kQRing = 8;                        // X chunk buffers (a power of two)
 constexpr int kQSpan = 4;                        // chunks one k-step may touch
 constexpr int kQInFlight = 2;                    // chunks in flight per loader wave
 constexpr int kQGran = 16;                       // 8-pixel granules per tile
 constexpr int kQCols = 8 * kQGran;               // pixel columns per tile
 constexpr int kQBlocks = kQCols / 32;            // MFMA column blocks
-constexpr int kQRowB = kQCols * 2;               // bytes per X row in LDS
-constexpr int kQBufB = kQKc * kQRowB;            // bytes per chunk buffer
-constexpr int kQCopies = kQBufB / 1024;          // 1 KB copies per chunk
+constexpr int kQRowB = kQCols * 2;               // bytes of one X row (one channel of the tile)
+constexpr int kQQuadB = 4 * kQRowB + 64;         // LDS bytes per 4 rows: quads of rows shift by 64 bytes of banks
+constexpr int kQBufB = (kQKc / 4) * kQQuadB;     // bytes per chunk buffer
+constexpr int kQCopies = kQKc / 4;               // 1 KB copies per chunk (4 rows each)
 constexpr int kQZeroOff = kQRing * kQBufB;       // a row of zeros after the ring
 constexpr int kQWin = 16;                        // kept blocks per window (one k-step)
-constexpr int kQWins = 6;                        // windows in a wave's ring
+constexpr int kQWins = 8;                        // windows in a wave's ring (a power of two)
 constexpr int kQRingE = kQWin * kQWins;          // ring entries
 constexpr int kQARowB = 64;                      // bytes of one block's weights (32 bf16)
 constexpr int32_t kQNever = 0x3fffffff;
@@ -134,30 +138,32 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
         // loader wave l copies the chunks with s % kQLoaders == l, up to
         // kQInFlight at a time, and marks each in sFlag once it has landed.
         const int32_t ld = wave - kQWaves;
-        const v4i32 rX = buffer_rsrc(a.x, int32_t(int64_t(batch) * a.x_img * 2));
-        const int h = lane >> 4, q = lane & 15;            // row within a copy (= its rotation), slot
-        const int32_t gran = 4 * (((q >> 2) - h) & 3) + (q & 3);   // tile granule held by slot q
+        const int32_t xbytes = int32_t(int64_t(batch) * a.x_img * 2);
+        const v4i32 rX = buffer_rsrc(a.x, xbytes);
+        // Lane l copies granule l mod 16 (8 pixels, 16 bytes) of row l / 16
+        // of each 4-row copy.
+        const int h = lane >> 4, gran = lane & 15;
         const int32_t rowb = a.HWo * 2;                    // bytes between channels
         const int32_t total_seq = nloc * nchunks;
-        int32_t pbase = 0, cur_k = -1;
+        uint32_t pbase = 0;
+        int32_t cur_k = -1;
         auto issue = [&](int32_t s) {
             const int32_t k = s / nchunks, c = s - k * nchunks;
             if (k != cur_k) {
                 cur_k = k;
                 const int32_t tile = (L + k * a.total) / gsets;
                 const int32_t id = tile * kQGran + gran;
-                pbase = 0;
+                pbase = uint32_t(xbytes);   // past the last image: the copies read zeros
                 if (id < ngran) {
                     const int32_t b = id / gpi, j = id - b * gpi;
-                    pbase = int32_t(int64_t(b) * a.x_img * 2) + 16 * j;
+                    pbase = uint32_t(int64_t(b) * a.x_img * 2) + 16 * j;
                 }
             }
-            const lds_char* dst = lx + (s % kQRing) * kQBufB;
-            const int32_t ch0 = c * kQKc + h;
+            const lds_char* dst = lx + (s & (kQRing - 1)) * kQBufB;
 #pragma unroll
             for (int i = 0; i < kQCopies; ++i) {
-                const int32_t ch = min(ch0 + 4 * i, a.m - 1);   // rows past m copy a real row (never read)
-                copy16_to_lds(rX, dst + i * 1024, pbase + ch * rowb, 0);
+                const int32_t ch = min(c * kQKc + 4 * i + h, a.m - 1);   // rows past m copy a real row (never read)
+                copy16_to_lds(rX, dst + i * kQQuadB, int32_t(pbase + uint32_t(ch * rowb)), 0);
             }
         };
         auto min_need = [&]() {
@@ -181,7 +187,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             }
             if (inflight == 2) vm_wait<kQCopies>();
             else vm_wait<0>();
-            if (lane == 0) lds_flag_store(&sFlag[oldest % kQRing], oldest);
+            if (lane == 0) lds_flag_store(&sFlag[oldest & (kQRing - 1)], oldest);
             oldest += kQLoaders;
             --inflight;
         }
@@ -224,7 +230,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             auto issue_windows = [&](int32_t upto) {   // windows [wi, min(upto, nwin))
                 upto = min(upto, nwin);
                 for (; wi < upto; ++wi) {
-                    const int32_t slot = wi % kQWins;
+                    const int32_t slot = wi & (kQWins - 1);
                     copy16_to_lds(rA, myA + slot * (kQWin * kQARowB), lane * 16 + (zb + wi * kQWin) * kQARowB, 0);
                     if (lane < kQWin)
                         copy4_to_lds(rI, (const lds_char*)myI + slot * (kQWin * 4), lane * 4 + (zb + wi * kQWin) * 4, 0);
@@ -238,16 +244,16 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             // Channel indices for the step at rz: pl (lanes < 16: entry rz +
             // lane), o1 / o2 (entry rz + k1 / rz + k1 + 4).
             auto plan_reads = [&](int32_t rz, int32_t& pl, int32_t& o1, int32_t& o2) {
-                pl = myI[(rz + (lane & 15)) % kQRingE];
-                o1 = myI[(rz + k1) % kQRingE];
-                o2 = myI[(rz + k1 + 4) % kQRingE];
+                pl = myI[(rz + (lane & 15)) & (kQRingE - 1)];
+                o1 = myI[(rz + k1) & (kQRingE - 1)];
+                o2 = myI[(rz + k1 + 4) & (kQRingE - 1)];
             };
             auto plan = [&](int32_t rz, int32_t pl) {
                 QStep st;
                 st.rz = rz;
                 const bool inE = lane < kQWin && rz + lane < nE;
                 const bool okc = inE && pl >= 0 && pl < a.m;
-                const int32_t sq = okc ? seq_base + (pl >> kQKcShift) : -1;
+                const int32_t sq = seq_base + (pl >> kQKcShift);
                 const int32_t avail = __builtin_popcountll(__ballot(inE));
                 const uint64_t mv = __ballot(okc);
                 if (mv == 0) {
@@ -258,29 +264,28 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 st.smin = __builtin_amdgcn_readlane(sq, __builtin_ctzll(mv));
                 const uint64_t far = __ballot(okc && sq > st.smin + (kQSpan - 1));
                 st.len = min(avail, far ? int32_t(__builtin_ctzll(far)) : 64);
-                const bool in_step = okc && lane < st.len;
-                int32_t top = st.smin;
-#pragma unroll
-                for (int d = 1; d < kQSpan; ++d)
-                    if (__ballot(in_step && sq == st.smin + d)) top = st.smin + d;
-                st.smax = top;
+                // Channels ascend within a col-group, so the step's last
+                // valid entry has its highest chunk.
+                const uint64_t in_step = st.len >= 64 ? mv : mv & ((uint64_t(1) << st.len) - 1);
+                st.smax = __builtin_amdgcn_readlane(sq, 63 - __builtin_clzll(in_step));
                 return st;
             };
             // LDS addresses of one lane's entry (k1 + 4 hh) for a step: its A
-            // row and its X row (column blocks rotated by rot), or the zero row.
+            // row and its X row (the four column blocks follow at 64-byte
+            // steps), or the zero row.
             struct Addr {
                 const lds_char* ap;
-                int32_t xoff, rot;
+                int32_t xoff;
             };
             auto addr = [&](const QStep& st, int32_t ch, int hh) {
                 Addr r;
                 const int32_t e = k1 + 4 * hh;
-                const bool ok = e < st.len && ch >= 0 && ch < a.m;
+                const bool ok = e < st.len && uint32_t(ch) < uint32_t(a.m);
                 const int32_t row = ch & (kQKc - 1);
-                r.xoff = ok ? ((seq_base + (ch >> kQKcShift)) % kQRing) * kQBufB + row * kQRowB + colb
+                r.xoff = ok ? ((seq_base + (ch >> kQKcShift)) & (kQRing - 1)) * kQBufB + (row >> 2) * kQQuadB +
+                                  (row & 3) * kQRowB + colb
                             : kQZeroOff + colb;
-                r.rot = ok ? (row & 3) : 0;
-                r.ap = ok ? myA + ((st.rz + e) % kQRingE) * kQARowB + colb : zrow + colb;
+                r.ap = ok ? myA + ((st.rz + e) & (kQRingE - 1)) * kQARowB + colb : zrow + colb;
                 return r;
             };
             // Waits until the chunks [smin, smax] of a step have landed.  A
@@ -290,7 +295,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
             // never waited for: the wave may have released them unseen.
             auto wait_landed = [&](const QStep& st) {
                 for (landed = max(landed, st.smin); landed <= st.smax;) {
-                    if (__builtin_amdgcn_readfirstlane(lds_flag_load(&sFlag[landed % kQRing])) >= landed) ++landed;
+                    if (__builtin_amdgcn_readfirstlane(lds_flag_load(&sFlag[landed & (kQRing - 1)])) >= landed) ++landed;
                     else __builtin_amdgcn_s_sleep(1);
                 }
                 fence_compiler();
@@ -318,8 +323,8 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 ra[1] = tr_read(p2.ap);
 #pragma unroll
                 for (int blk = 0; blk < kQBlocks; ++blk) {
-                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * ((blk + p1.rot) & 3));
-                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * ((blk + p2.rot) & 3));
+                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * blk);
+                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * blk);
                 }
             }
             int32_t rz_next = cur.len;
@@ -353,8 +358,8 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
                 for (int blk = 0; blk < kQBlocks; ++blk) {
                     acc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, join(rb[blk][0], rb[blk][1]),
                                                                      acc[blk], 0, 0, 0);
-                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * ((blk + p1.rot) & 3));
-                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * ((blk + p2.rot) & 3));
+                    rb[blk][0] = tr_read(lx + p1.xoff + 64 * blk);
+                    rb[blk][1] = tr_read(lx + p2.xoff + 64 * blk);
                 }
                 if (has_next2) {
                     wait_windows(rz2);

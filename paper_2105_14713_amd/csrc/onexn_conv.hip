@@ -112,8 +112,7 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
-    if (pointwise_applies(a, xdt, ydt, layout) && !env_is("ONEXN_PW_KERNEL", "kxk"))
-        return launch_pointwise(a, xdt, ydt, s);
+    if (pointwise_applies(a, xdt, ydt, layout)) return launch_pointwise(a, xdt, ydt, s);
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     return launch_generic(a, xdt, ydt, s);
 }
