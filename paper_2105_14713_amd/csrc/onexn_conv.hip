@@ -114,5 +114,6 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
     if (pointwise_applies(a, xdt, ydt, layout)) return launch_pointwise(a, xdt, ydt, s);
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
+    if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     return launch_generic(a, xdt, ydt, s);
 }

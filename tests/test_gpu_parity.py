@@ -390,14 +390,15 @@ def test_kxk_matches_generic_on_random_fp32(monkeypatch):
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma", "pwfma"])
 def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
     t would put NaN into the output."""
     k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
                       "stream": (1, 32, 300, torch.float32, 12), "bf16": (1, 32, 96, torch.bfloat16, 12),
-                      "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12)}[kind]
+                      "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
+                      "pwfma": (1, 4, 30, torch.float32, 12)}[kind]
     if kind in ("tile", "stream"):
         monkeypatch.setenv("ONEXN_PW_KERNEL", kind)
     n = 3 * N + N // 2
@@ -415,3 +416,25 @@ def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     torch.cuda.synchronize()
     ref, _ = oracle_conv(w.float(), x.float(), N, 0.5, False, 1, pd)
     np.testing.assert_array_equal(y.double().cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("tile", ["1", "2", "3", "4", "5"])
+@pytest.mark.parametrize("case", [
+    dict(N=4, m=24, n=98, B=3, H=9, W=7),        # odd pixels per image, ragged last col-group
+    dict(N=8, m=1100, n=44, B=2, H=5, W=5),      # contractions longer than one staged window
+    dict(N=1, m=37, n=5, B=2, H=13, W=11),
+    dict(N=2, m=64, n=17, B=1, H=16, W=16),
+], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}")
+def test_pw_fma_integer_exact(case, tile, monkeypatch):
+    """The 1x1 FMA kernel at every tile shape (pixels per lane, col-groups per
+    workgroup, waves splitting a contraction), with a partial last set of
+    col-groups and p from dense to nearly empty."""
+    monkeypatch.setenv("ONEXN_FMA_TILE", tile)
+    c = case
+    w, x = workloads.gen_integer_layer(seed=c["m"] + c["N"], cout=c["n"], cin=c["m"], k=1,
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=1, xmax=2)
+    print(f"pw fma {c} tile={tile}", flush=True)
+    for p in (0.0, 0.5, 0.95):
+        y, _ = gpu_conv(w, x, c["N"], p, True, 1, 0)
+        ref, _ = oracle_conv(w, x, c["N"], p, True, 1, 0)
+        np.testing.assert_array_equal(y, ref)
