@@ -167,6 +167,8 @@ bool pw_bf16_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_
 onexn_status launch_pw_bf16(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
 bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 bool pw_fma_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+bool pw_direct_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_pw_direct(ConvArgs a, hipStream_t stream);
 onexn_status launch_pw_fma(ConvArgs a, hipStream_t stream);
 onexn_status launch_kxk(ConvArgs a, hipStream_t stream);
 

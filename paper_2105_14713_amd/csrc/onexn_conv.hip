@@ -112,7 +112,17 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
-    if (pointwise_applies(a, xdt, ydt, layout)) return launch_pointwise(a, xdt, ydt, s);
+    // fp32 1x1 layers: the LDS-tile pointwise kernels for layers that widen
+    // the channels over many pixels, the register-operand kernel for the
+    // rest (contractions at least as long as the output is wide, few pixels,
+    // any stride or padding).  ONEXN_PW_KERNEL=tile|stream|direct overrides.
+    const bool direct = pw_direct_applies(a, xdt, ydt, layout) && !generic_forced();
+    if (pointwise_applies(a, xdt, ydt, layout)) {
+        const bool forced_pw = env_is("ONEXN_PW_KERNEL", "tile") || env_is("ONEXN_PW_KERNEL", "stream");
+        const bool prefer_direct = env_is("ONEXN_PW_KERNEL", "direct") || a.m >= a.n || a.npix <= 8192;
+        if (!direct || forced_pw || !prefer_direct) return launch_pointwise(a, xdt, ydt, s);
+    }
+    if (direct) return launch_pw_direct(a, s);
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     return launch_generic(a, xdt, ydt, s);

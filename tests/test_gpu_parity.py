@@ -390,7 +390,7 @@ def test_kxk_matches_generic_on_random_fp32(monkeypatch):
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma", "pwfma"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma", "pwfma", "direct"])
 def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
@@ -398,8 +398,8 @@ def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
                       "stream": (1, 32, 300, torch.float32, 12), "bf16": (1, 32, 96, torch.bfloat16, 12),
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
-                      "pwfma": (1, 4, 30, torch.float32, 12)}[kind]
-    if kind in ("tile", "stream"):
+                      "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
+    if kind in ("tile", "stream", "direct"):
         monkeypatch.setenv("ONEXN_PW_KERNEL", kind)
     n = 3 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=7, cout=n, cin=m, k=k, batch=2, H=H, wmax=2, xmax=2)
@@ -437,4 +437,27 @@ def test_pw_fma_integer_exact(case, tile, monkeypatch):
     for p in (0.0, 0.5, 0.95):
         y, _ = gpu_conv(w, x, c["N"], p, True, 1, 0)
         ref, _ = oracle_conv(w, x, c["N"], p, True, 1, 0)
+        np.testing.assert_array_equal(y, ref)
+
+
+@pytest.mark.parametrize("tile", ["1", "2", "3", "4"])
+@pytest.mark.parametrize("case", [
+    dict(N=32, m=45, n=80, B=3, H=28, W=28, s=2, pd=0),   # strided 1x1 (downsample)
+    dict(N=16, m=300, n=56, B=2, H=15, W=9, s=2, pd=1),   # stride and padding
+    dict(N=32, m=700, n=40, B=2, H=7, W=7, s=1, pd=0),    # long contraction, few pixels
+    dict(N=16, m=33, n=20, B=1, H=10, W=13, s=3, pd=2),
+], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
+def test_pw_direct_integer_exact(case, tile, monkeypatch):
+    """The 1x1 kernel with register-loaded operands at every tile shape
+    (column blocks per unit, waves splitting the contraction): strides,
+    padding, ragged col-groups and pixel tails, p from dense to nearly empty."""
+    monkeypatch.setenv("ONEXN_DIRECT_TILE", tile)
+    monkeypatch.setenv("ONEXN_PW_KERNEL", "direct")
+    c = case
+    w, x = workloads.gen_integer_layer(seed=c["m"] + c["n"], cout=c["n"], cin=c["m"], k=1,
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=1, xmax=2)
+    print(f"pw direct {c} tile={tile}", flush=True)
+    for p in (0.0, 0.5, 0.95):
+        y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
         np.testing.assert_array_equal(y, ref)
