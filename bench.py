@@ -65,16 +65,15 @@ def layer_work(layer, packed, batch, dtype, out_dtype):
     return f_act, f_dense, b_x + b_y + b_w
 
 
-def kernel_source_hash():
-    """sha256 over the library's kernel sources: traffic counters taken on an
-    older build are not reported for a newer one."""
+def source_hash(files):
+    """sha256 over the named source files (paths relative to the repository
+    root): byte counters taken on an older build of a kernel are not reported
+    for a newer one."""
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2105_14713_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            h.update(name.encode())
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(f.read())
+    for name in sorted(files):
+        h.update(name.encode())
+        with open(os.path.join(ROOT, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
@@ -82,16 +81,20 @@ def measured_traffic(workload):
     """HBM bytes per launch of the workload's kernel from the committed
     rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE in KiB per dispatch,
     each scaled by the factor the same counter shows for a copy kernel of
-    known size), or None when there is none for the current kernel sources."""
+    known size), or None when there is none, or when any source file the
+    kernel is built from (listed in the record) has changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha256") != kernel_source_hash():
-        return None
     w = rec.get("workloads", {}).get(workload)
     if not w:
+        return None
+    try:
+        if w.get("source_sha256") != source_hash(w["sources"]):
+            return None
+    except (OSError, KeyError):
         return None
     return 1024.0 * (w["fetch_kib"] * rec["fetch_scale"] + w["write_kib"] * rec["write_scale"])
 
