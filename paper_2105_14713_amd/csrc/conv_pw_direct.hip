@@ -24,11 +24,12 @@
 // kept blocks (contiguous ranges) and add their partial sums through LDS at
 // the end, for layers with few pixels and long col-groups.
 //
-// Pipelining.  Steps are taken in batches of kDB: a batch's channel indices
-// come in one lane-parallel load, its weight and input loads are all issued
-// before the previous batch's MFMAs, so a wave keeps two batches of loads in
-// flight.  Entries past the wave's range and channels outside [0, m) read
-// zeros (out-of-range buffer offsets), so they add nothing.
+// Pipelining.  Steps are taken in batches of kDB: channel indices come in
+// lane-parallel windows of 64 entries loaded a window ahead, a batch's
+// weight and input loads are all issued before the previous batch's MFMAs,
+// so a wave keeps two batches of loads in flight.  Entries past the wave's
+// range and channels outside [0, m) read zeros (out-of-range buffer offsets),
+// so they add nothing.
 #include <cstdlib>
 
 #include "lds_copy.h"
@@ -105,19 +106,29 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
         float av[kDB];
         float bv[kDB][NB];
     };
-    // Loads of the batch starting at entry z: lane l's channel index is
-    // entry z + l (l < kDB * KS); step s hands entry z + s*KS + kk to the
-    // lane with ds_bpermute.
+    // Channel indices come in windows of 64 entries (lane j: entry wbase + j),
+    // loaded a window ahead of use, so a batch's input addresses never wait
+    // for an index load.  Entries at or past z1 and channels outside [0, m)
+    // read zeros.
+    constexpr int E = kDB * KS;   // entries per batch (divides 64)
+    static_assert(64 % E == 0, "batches tile the index windows");
+    auto load_idx = [&](int32_t z) { return int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, (z + lane) * 4, 0, 0)); };
+    int32_t wbase = z0;
+    int32_t ivw = load_idx(z0), ivn = load_idx(z0 + 64);
     auto issue = [&](Batch& bt, int32_t z) {
-        const int32_t iv = __builtin_amdgcn_raw_buffer_load_b32(rI, (z + lane) * 4, 0, 0);
-        const bool in = z + lane < z1;
-        const int32_t chv = (in && uint32_t(iv) < uint32_t(a.m)) ? iv : -1;
+        if (z - wbase >= 64) {
+            wbase += 64;
+            ivw = ivn;
+            ivn = load_idx(wbase + 64);
+        }
+        const int32_t off = z - wbase;
 #pragma unroll
         for (int st = 0; st < kDB; ++st) {
             const int32_t ze_ = z + st * KS;
             bt.av[st] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, (ze_ * N + lane) * 4, 0, 0));
-            const int32_t ch = __builtin_amdgcn_ds_bpermute(4 * (st * KS + kk), chv);
-            const uint32_t choff = ch >= 0 ? uint32_t(ch) * chb : xbytes;
+            const int32_t ch = __builtin_amdgcn_ds_bpermute(4 * (off + st * KS + kk), ivw);
+            const bool ok = ze_ + kk < z1 && uint32_t(ch) < uint32_t(a.m);
+            const uint32_t choff = ok ? uint32_t(ch) * chb : xbytes;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
                 bt.bv[st][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
@@ -131,15 +142,15 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
             for (int nb = 0; nb < NB; ++nb) acc[nb] = M::step(bt.av[st], bt.bv[st][nb], acc[nb]);
     };
 
-    const int32_t nbat = (z1 - z0 + kDB * KS - 1) / (kDB * KS);
+    const int32_t nbat = (z1 - z0 + E - 1) / E;
     if (nbat > 0) {
         Batch b0, b1;
         issue(b0, z0);
         for (int32_t bi = 0; bi < nbat; bi += 2) {
-            if (bi + 1 < nbat) issue(b1, z0 + (bi + 1) * kDB * KS);
+            if (bi + 1 < nbat) issue(b1, z0 + (bi + 1) * E);
             consume(b0);
             if (bi + 1 >= nbat) break;
-            if (bi + 2 < nbat) issue(b0, z0 + (bi + 2) * kDB * KS);
+            if (bi + 2 < nbat) issue(b0, z0 + (bi + 2) * E);
             consume(b1);
         }
     }
