@@ -27,15 +27,25 @@ namespace {
 // fma_conv: N <= 8.
 // ---------------------------------------------------------------------------
 
-template <int N, int PPT, bool kUnit, typename TX, typename TY>
+// KS > 1 splits each col-group's contraction over KS slices of the
+// workgroup (whole waves each), for layers with few output pixels and long
+// col-groups; the slices' partial sums are added through LDS.
+template <int N, int PPT, int KS, bool kUnit, typename TX, typename TY>
 __global__ void __launch_bounds__(kThreads) fma_conv(ConvArgs a) {
     constexpr int U = 8;   // kappa per batch: U * PPT gathered loads in flight per lane
+    constexpr int TPS = kThreads / KS;   // threads per contraction slice
+    static_assert(TPS % 64 == 0, "a slice is whole waves");
+    __shared__ float sR[KS > 1 ? (KS - 1) * TPS * PPT * N : 1];
     const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
     const int32_t g = L % a.G;
     const int32_t tile = L / a.G;
+    const int kq = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / TPS);
+    const int pt = int(threadIdx.x) % TPS;
     int32_t zb, ze;
     group_range(a, g, zb, ze);
     const int32_t Kg = (ze - zb) * a.KK;
+    const int32_t per = (Kg + KS - 1) / KS;
+    const int32_t kbeg = min(Kg, kq * per), kend = min(Kg, kbeg + per);
 
     const TX* __restrict__ x = static_cast<const TX*>(a.x);
     const TX* __restrict__ D = static_cast<const TX*>(a.D);
@@ -43,18 +53,18 @@ __global__ void __launch_bounds__(kThreads) fma_conv(ConvArgs a) {
     float acc[PPT][N];
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
-        pp[i] = pixel_pos(a, tile * (kThreads * PPT) + i * kThreads + int32_t(threadIdx.x));
+        pp[i] = pixel_pos(a, tile * (TPS * PPT) + i * TPS + pt);
 #pragma unroll
         for (int o = 0; o < N; ++o) acc[i][o] = 0.f;
     }
 
-    KapWalk w = walk_at<kUnit>(a, 0);
-    for (int32_t k0 = 0; k0 < Kg; k0 += U) {
+    KapWalk w = walk_at<kUnit>(a, kbeg);
+    for (int32_t k0 = kbeg; k0 < kend; k0 += U) {
         int32_t cs[U];
         KapWalk ws[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            cs[u] = walk_channel(a, w, zb, ze, k0 + u < Kg);
+            cs[u] = walk_channel(a, w, zb, ze, k0 + u < kend);
             ws[u] = w;
             walk_step<kUnit>(a, w);
         }
@@ -77,6 +87,23 @@ __global__ void __launch_bounds__(kThreads) fma_conv(ConvArgs a) {
 #pragma unroll
                 for (int o = 0; o < N; ++o) acc[i][o] = fmaf(wv[o], xv[u][i], acc[i][o]);
         }
+    }
+
+    if constexpr (KS > 1) {
+        if (kq > 0) {
+#pragma unroll
+            for (int i = 0; i < PPT; ++i)
+#pragma unroll
+                for (int o = 0; o < N; ++o) sR[(((kq - 1) * PPT + i) * N + o) * TPS + pt] = acc[i][o];
+        }
+        __syncthreads();
+        if (kq > 0) return;
+#pragma unroll
+        for (int k = 1; k < KS; ++k)
+#pragma unroll
+            for (int i = 0; i < PPT; ++i)
+#pragma unroll
+                for (int o = 0; o < N; ++o) acc[i][o] += sR[(((k - 1) * PPT + i) * N + o) * TPS + pt];
     }
 
     TY* __restrict__ y = static_cast<TY*>(a.y);
@@ -292,6 +319,17 @@ onexn_status launch_typed(ConvArgs a, hipStream_t stream) {
     auto grid_for = [&](int64_t pt) { return ((npix + pt - 1) / pt) * a.G; };
     const int64_t big_grid_min = 2 * 256;   // aim for >= 2 workgroups per CU
     auto go = [&](auto kernel, int64_t pt) { return launch_grid(kernel, a, grid_for(pt), stream); };
+    // N <= 8: several pixels per lane when the grid is large, one pixel per
+    // lane next, and for small grids 64-pixel tiles with the contraction split
+    // over the four waves (if each slice keeps at least a few batches).
+    auto go_fma = [&](auto n_const) {
+        constexpr int NN = decltype(n_const)::value;
+        constexpr int WIDE = NN == 8 ? 2 : 4;
+        if (grid_for(256 * WIDE) >= big_grid_min) return go(fma_conv<NN, WIDE, 1, kUnit, TX, TY>, 256 * WIDE);
+        const int64_t kg = a.G > 0 ? int64_t(a.t) / a.G * a.KK : 0;
+        if (grid_for(256) >= big_grid_min || kg < 4 * 8 * 4) return go(fma_conv<NN, 1, 1, kUnit, TX, TY>, 256);
+        return go(fma_conv<NN, 1, 4, kUnit, TX, TY>, 64);
+    };
     switch (a.N) {
         case 16:
             if (grid_for(256) >= big_grid_min) return go(mfma_conv<16, 64, kUnit, TX, TY>, 256);
@@ -299,18 +337,10 @@ onexn_status launch_typed(ConvArgs a, hipStream_t stream) {
         case 32:
             if (grid_for(256) >= big_grid_min) return go(mfma_conv<32, 64, kUnit, TX, TY>, 256);
             return go(mfma_conv<32, 32, kUnit, TX, TY>, 128);
-        case 1:
-            if (grid_for(1024) >= big_grid_min) return go(fma_conv<1, 4, kUnit, TX, TY>, 1024);
-            return go(fma_conv<1, 1, kUnit, TX, TY>, 256);
-        case 2:
-            if (grid_for(1024) >= big_grid_min) return go(fma_conv<2, 4, kUnit, TX, TY>, 1024);
-            return go(fma_conv<2, 1, kUnit, TX, TY>, 256);
-        case 4:
-            if (grid_for(1024) >= big_grid_min) return go(fma_conv<4, 4, kUnit, TX, TY>, 1024);
-            return go(fma_conv<4, 1, kUnit, TX, TY>, 256);
-        case 8:
-            if (grid_for(512) >= big_grid_min) return go(fma_conv<8, 2, kUnit, TX, TY>, 512);
-            return go(fma_conv<8, 1, kUnit, TX, TY>, 256);
+        case 1: return go_fma(std::integral_constant<int, 1>());
+        case 2: return go_fma(std::integral_constant<int, 2>());
+        case 4: return go_fma(std::integral_constant<int, 4>());
+        case 8: return go_fma(std::integral_constant<int, 8>());
     }
     return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: N=%d is not supported", a.N);
 }

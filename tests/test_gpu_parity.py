@@ -83,6 +83,15 @@ def test_bf16(N, kshape, layout, out_dtype):
         assert err <= 1e-5
 
 
+def test_fma_split_contraction_bf16_nhwc():
+    """The N <= 8 generic kernel with its contraction split over waves, on bf16
+    NHWC input (small integers: exact in bf16 and in fp32 accumulation)."""
+    w, x = workloads.gen_integer_layer(seed=77, cout=18, cin=64, k=3, batch=1, H=12, wmax=2, xmax=2)
+    y, _ = gpu_conv(w.bfloat16(), x.bfloat16(), 4, 0.5, True, 1, 1, "nhwc", torch.float32)
+    ref, _ = oracle_conv(w, x, 4, 0.5, True, 1, 1)
+    np.testing.assert_array_equal(y, ref)
+
+
 def test_bf16_integer_exact():
     """Small integers are exact in bf16, so bf16 -> fp32 output must be bit-exact."""
     for N in (8, 16, 32):
@@ -132,6 +141,9 @@ def test_batch_zero_is_noop():
     dict(n=48, m=7, k=5, N=16, B=2, H=9, s=3, pd=2),     # 5x5, stride 3
     dict(n=8, m=3, k=16, N=8, B=1, H=20, s=8, pd=15),    # largest kernel, stride and pad
     dict(n=20, m=2, k=16, N=16, B=2, H=17, s=8, pd=15),  # the same on the MFMA kernel
+    dict(n=18, m=64, k=3, N=4, B=1, H=12, s=1, pd=1),    # few pixels, long col-groups: split contraction
+    dict(n=20, m=40, k=3, N=8, B=1, H=9, s=2, pd=1),     # the same at N = 8, stride 2
+    dict(n=7, m=70, k=3, N=1, B=1, H=6, s=1, pd=0),      # and at N = 1
 ])
 def test_edge_shapes_integer_exact(case):
     c = case
