@@ -10,8 +10,8 @@
 // multiply-adds.  A 16-row matrix-core tile would be at least half padding at
 // these N.
 //
-// Work split.  A workgroup computes one pixel tile (64 lanes x PPT pixels,
-// 64 apart) for a set of GSW col-groups: wave w takes col-group w % GSW of the
+// Work split.  A workgroup computes a run of pixel tiles (64 lanes x PPT
+// pixels each: 64 apart, or 4 consecutive ones) for a set of GSW col-groups: wave w takes col-group w % GSW of the
 // set and, when the contraction is split (KSPLIT = 4 / GSW waves per
 // col-group, for layers with few pixels and long col-groups), a contiguous
 // share of its kept blocks; the partial sums of a split are added through LDS
@@ -36,8 +36,11 @@ namespace {
 constexpr int kFThreads = 256;
 constexpr int kFWin = 256;   // kept blocks per staged window (per wave)
 
-template <int N, int PPT, int GSW>
+// V4: a lane owns 4 consecutive pixels (pixels per image a multiple of 4,
+// 16-byte aligned x and y), read and written with 16-byte accesses.
+template <int N, int PPT, int GSW, bool V4>
 __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
+    static_assert(!V4 || PPT == 4, "4 consecutive pixels per lane");
     constexpr int KSPLIT = 4 / GSW;
     constexpr int TP = 64 * PPT;           // pixels per tile
     constexpr int RED = KSPLIT > 1 ? 4 * N * PPT * 64 : 1;
@@ -50,8 +53,14 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     const int gw = wave % GSW, kq = wave / GSW;
     const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
     const int32_t gsets = (a.G + GSW - 1) / GSW;
-    const int32_t tile = L / gsets;
-    const int32_t g = (L - tile * gsets) * GSW + gw;
+    // The workgroup's col-group set and its run of pixel tiles: the grid is
+    // gsets x (tile runs), and a run is ceil(tiles / runs) tiles long.
+    const int32_t ntiles = (a.npix + TP - 1) / TP;
+    const int32_t nruns = a.total / gsets;
+    const int32_t tpw = (ntiles + nruns - 1) / nruns;
+    const int32_t run = L / gsets;
+    const int32_t t0 = run * tpw, t1 = min(ntiles, t0 + tpw);
+    const int32_t g = (L - run * gsets) * GSW + gw;
     int32_t zb = 0, ze = 0;
     if (g < a.G) group_range(a, g, zb, ze);
     // This wave's contiguous share of the col-group's kept blocks.
@@ -60,20 +69,6 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     const int32_t batch = a.npix / a.HWo;
     const int32_t xbytes = int32_t(int64_t(batch) * a.x_img * 4);
 
-    uint32_t xo[PPT];   // byte offset of the lane's pixels at channel 0 (past the input: invalid)
-    int64_t yo[PPT];    // element offset in y at channel 0, or -1
-#pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-        const int32_t p = tile * TP + i * 64 + lane;
-        xo[i] = uint32_t(xbytes);
-        yo[i] = -1;
-        if (p < a.npix) {
-            const int32_t b = p / a.HWo, hw = p - b * a.HWo;
-            xo[i] = uint32_t((int64_t(b) * a.x_img + hw) * 4);
-            yo[i] = int64_t(b) * a.y_img + hw;
-        }
-    }
-
     const __amdgpu_buffer_rsrc_t rX =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.x), 0, xbytes, kRawBufferFlags);
     const v4i32 rI = buffer_rsrc(a.I, z1 * 4);
@@ -81,18 +76,16 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     const int32_t* const wI = sI[wave];
     const float* const wD = sD[wave];
 
+    uint32_t xo[PPT];   // byte offset of the lane's pixels at channel 0 (past the input: invalid)
+    int64_t yo[PPT];    // element offset in y at channel 0, or -1
     float acc[N][PPT];
-#pragma unroll
-    for (int o = 0; o < N; ++o)
-#pragma unroll
-        for (int i = 0; i < PPT; ++i) acc[o][i] = 0.f;
 
     // Blocks are taken in batches of kFB: lane j < kFB of the wave reads
     // block j's channel, every lane then issues the batch's input loads at
     // once, and the next batch's loads are issued before this batch's
-    // multiply-adds, so a wave keeps up to 2 kFB PPT loads in flight (kFB
-    // shrinks as PPT grows, to keep the register count and occupancy).
-    constexpr int kFB = PPT >= 4 ? 4 : 16 / PPT;   // loads per batch stay at 16 (or fewer)
+    // multiply-adds, so a wave keeps up to 2 kFB loads in flight (kFB shrinks
+    // as the loads widen, to keep the register count and occupancy).
+    constexpr int kFB = V4 ? 8 : (PPT >= 4 ? 4 : 16 / PPT);
     struct Batch {
         float xv[kFB][PPT];
     };
@@ -100,21 +93,27 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     // value 0 (their loads stay inside the input), so a partial batch adds
     // nothing; the window's weights past the share are zeros (range-checked
     // copies of whole 64-entry blocks).
-    auto issue = [&](Batch& bt, int32_t e, int32_t cnt) {
+    auto issue = [&](Batch& bt, int32_t e, int32_t cnt) __attribute__((always_inline)) {
         const int32_t chv = wI[e + (lane & (kFB - 1))];
 #pragma unroll
         for (int j = 0; j < kFB; ++j) {
             const int32_t ch = __builtin_amdgcn_readlane(chv, j);
             const bool ok = j < cnt && uint32_t(ch) < uint32_t(a.m);
             const int32_t choff = ok ? ch * a.HWo * 4 : 0;
+            if constexpr (V4) {
+                const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rX, int32_t(xo[0]), choff, 0));
 #pragma unroll
-            for (int i = 0; i < PPT; ++i) {
-                const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rX, int32_t(xo[i]), choff, 0));
-                bt.xv[j][i] = ok ? v : 0.f;
+                for (int i = 0; i < 4; ++i) bt.xv[j][i] = ok ? v[i] : 0.f;
+            } else {
+#pragma unroll
+                for (int i = 0; i < PPT; ++i) {
+                    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rX, int32_t(xo[i]), choff, 0));
+                    bt.xv[j][i] = ok ? v : 0.f;
+                }
             }
         }
     };
-    auto consume = [&](const Batch& bt, int32_t e) {
+    auto consume = [&](const Batch& bt, int32_t e) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < kFB; ++j) {
 #pragma unroll
@@ -125,14 +124,15 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
             }
         }
     };
-
-    for (int32_t w0 = z0; w0 < z1; w0 += kFWin) {
-        const int32_t nw = min(kFWin, z1 - w0);
+    // Stages entries [w0, w0 + nw) of the wave's share into its LDS window.
+    auto stage = [&](int32_t w0, int32_t nw) __attribute__((always_inline)) {
         for (int32_t e0 = 0; e0 < nw; e0 += 64)
             copy4_to_lds(rI, (const lds_char*)(wI + e0), (w0 + e0 + lane) * 4, 0);
         for (int32_t e0 = 0; e0 < nw * N; e0 += 64)
             copy4_to_lds(rD, (const lds_char*)(wD + e0), (w0 * N + e0 + lane) * 4, 0);
         vm_wait<0>();   // the window is in this wave's LDS
+    };
+    auto compute_window = [&](int32_t nw) __attribute__((always_inline)) {
         const int32_t nb = (nw + kFB - 1) / kFB;
         auto cnt = [&](int32_t bi) { return min(kFB, nw - bi * kFB); };
         Batch b0, b1;
@@ -144,41 +144,94 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
             if (bi + 2 < nb) issue(b0, (bi + 2) * kFB, cnt(bi + 2));
             consume(b1, (bi + 1) * kFB);
         }
-        wait_lgkm();    // this wave's reads of the window are done before it is refilled
-    }
+    };
 
-    if constexpr (KSPLIT > 1) {
-#pragma unroll
-        for (int o = 0; o < N; ++o)
-#pragma unroll
-            for (int i = 0; i < PPT; ++i) sR[((wave * N + o) * PPT + i) * 64 + lane] = acc[o][i];
-        __syncthreads();
-        if (kq != 0) return;
-#pragma unroll
-        for (int o = 0; o < N; ++o)
-#pragma unroll
-            for (int i = 0; i < PPT; ++i)
-#pragma unroll
-                for (int k = 1; k < KSPLIT; ++k) acc[o][i] += sR[(((wave + k * GSW) * N + o) * PPT + i) * 64 + lane];
-    }
-    if (g >= a.G) return;
+    // A share that fits one window is staged once for all the run's tiles.
+    const bool one_window = z1 - z0 <= kFWin;
+    if (one_window && z1 > z0) stage(z0, z1 - z0);
 
     float* __restrict__ y = static_cast<float*>(a.y);
+    for (int32_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
-    for (int o = 0; o < N; ++o) {
-        const int32_t oc = g * N + o;
-        if (oc >= a.n) continue;
+        for (int i = 0; i < PPT; ++i) {
+            const int32_t p = V4 ? tile * TP + lane * 4 + i : tile * TP + i * 64 + lane;
+            xo[i] = uint32_t(xbytes);
+            yo[i] = -1;
+            if (p < a.npix) {
+                const int32_t b = p / a.HWo, hw = p - b * a.HWo;
+                xo[i] = uint32_t((int64_t(b) * a.x_img + hw) * 4);
+                yo[i] = int64_t(b) * a.y_img + hw;
+            }
+        }
 #pragma unroll
-        for (int i = 0; i < PPT; ++i)
-            if (yo[i] >= 0) y[yo[i] + int64_t(oc) * a.y_c] = acc[o][i];
+        for (int o = 0; o < N; ++o)
+#pragma unroll
+            for (int i = 0; i < PPT; ++i) acc[o][i] = 0.f;
+
+        if (one_window) {
+            if (z1 > z0) compute_window(z1 - z0);
+        } else {
+            for (int32_t w0 = z0; w0 < z1; w0 += kFWin) {
+                const int32_t nw = min(kFWin, z1 - w0);
+                stage(w0, nw);
+                compute_window(nw);
+                wait_lgkm();    // this wave's reads of the window are done before it is refilled
+            }
+        }
+
+        if constexpr (KSPLIT > 1) {
+#pragma unroll
+            for (int o = 0; o < N; ++o)
+#pragma unroll
+                for (int i = 0; i < PPT; ++i) sR[((wave * N + o) * PPT + i) * 64 + lane] = acc[o][i];
+            __syncthreads();
+            if (kq == 0) {
+#pragma unroll
+                for (int o = 0; o < N; ++o)
+#pragma unroll
+                    for (int i = 0; i < PPT; ++i)
+#pragma unroll
+                        for (int k = 1; k < KSPLIT; ++k)
+                            acc[o][i] += sR[(((wave + k * GSW) * N + o) * PPT + i) * 64 + lane];
+            }
+            __syncthreads();   // sR is free for the next tile
+        }
+        if (kq != 0 || g >= a.G) continue;
+
+#pragma unroll
+        for (int o = 0; o < N; ++o) {
+            const int32_t oc = g * N + o;
+            if (oc >= a.n) continue;
+            if constexpr (V4) {
+                if (yo[0] >= 0) {
+                    const f32x4 v = {acc[o][0], acc[o][1], acc[o][2], acc[o][3]};
+                    *reinterpret_cast<f32x4*>(y + yo[0] + int64_t(oc) * a.y_c) = v;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < PPT; ++i)
+                    if (yo[i] >= 0) y[yo[i] + int64_t(oc) * a.y_c] = acc[o][i];
+            }
+        }
     }
 }
 
+// Tiles per workgroup: as many as keep at least 8 workgroups per compute
+// unit (at most 16), so that layers with many pixels stage their indices and
+// weights once per run of tiles.
 template <int N, int PPT, int GSW>
 onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
-    const int64_t tiles = (int64_t(a.npix) + 64 * PPT - 1) / (64 * PPT);
+    const int64_t ntiles = (int64_t(a.npix) + 64 * PPT - 1) / (64 * PPT);
     const int64_t gsets = (a.G + GSW - 1) / GSW;
-    return launch_grid(pw_fma<N, PPT, GSW>, a, tiles * gsets, s, kFThreads);
+    int64_t tpw = std::max<int64_t>(1, std::min<int64_t>(16, ntiles * gsets / (8 * int64_t(device_cu_count()))));
+    if (const char* env = std::getenv("ONEXN_FMA_TPW")) tpw = std::max(1, std::atoi(env));   // testing
+    const int64_t tiles = (ntiles + tpw - 1) / tpw;   // tile runs
+    if constexpr (PPT == 4) {
+        const bool v4 = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
+                        (reinterpret_cast<uintptr_t>(a.y) & 15) == 0 && !std::getenv("ONEXN_FMA_NO_V4");
+        if (v4) return launch_grid(pw_fma<N, PPT, GSW, true>, a, tiles * gsets, s, kFThreads);
+    }
+    return launch_grid(pw_fma<N, PPT, GSW, false>, a, tiles * gsets, s, kFThreads);
 }
 
 // Tile shapes (pixels per lane, col-groups per workgroup): four col-groups

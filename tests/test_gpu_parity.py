@@ -436,6 +436,8 @@ def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     dict(N=8, m=1100, n=44, B=2, H=5, W=5),      # contractions longer than one staged window
     dict(N=1, m=37, n=5, B=2, H=13, W=11),
     dict(N=2, m=64, n=17, B=1, H=16, W=16),
+    dict(N=4, m=20, n=50, B=3, H=12, W=10),      # pixels per image a multiple of 4 (16-byte path)
+    dict(N=8, m=16, n=72, B=5, H=28, W=28),
 ], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}")
 def test_pw_fma_integer_exact(case, tile, monkeypatch):
     """The 1x1 FMA kernel at every tile shape (pixels per lane, col-groups per
