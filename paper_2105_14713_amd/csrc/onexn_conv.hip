@@ -111,6 +111,7 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
         a.y_pix = n;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (pw_bf16r_applies(a, xdt, ydt, layout) && !env_is("ONEXN_PWB_KERNEL", "queue")) return launch_pw_bf16r(a, ydt, s);
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
     // fp32 1x1 layers: the LDS-tile pointwise kernels for layers that widen
     // the channels over many pixels, the register-operand kernel for the

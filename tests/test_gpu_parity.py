@@ -332,28 +332,35 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
         np.testing.assert_array_equal(y, ref)
 
 
-@pytest.mark.parametrize("wgs", ["1", "7", "default"])
+@pytest.mark.parametrize("variant", ["reg2", "reg4", "reg6", "queue1", "queue7", "queue"])
 @pytest.mark.parametrize("shape", [
     dict(m=300, B=3, H=14, W=14),    # 5 channel chunks (ragged last), partial last granule per image
     dict(m=64, B=2, H=12, W=12),     # one chunk, whole granules, tiles across images
     dict(m=45, B=1, H=4, W=3),       # fewer pixels than one tile
-    dict(m=700, B=1, H=8, W=6),      # long contraction
-], ids=["m300", "m64", "m45", "m700"])
-def test_pw_bf16_integer_exact(shape, wgs, monkeypatch):
-    """The bf16 pointwise kernel (1x1, N = 32, pixels per image a multiple of
-    4): small integers are exact in bf16 and in fp32 accumulation, so fp32
-    output is bit-exact and bf16 output equals the oracle rounded to bf16.
-    Covers ragged col-groups and a partial last set of 8 col-groups (n = 304),
-    dense to nearly empty col-groups (p = 0, 0.5, 0.97: steps cut short where
-    16 kept channels span more chunks than LDS holds), and workgroup counts
-    that give each workgroup several work items."""
-    if wgs != "default":
-        monkeypatch.setenv("ONEXN_PWB_WGS", wgs)
+    dict(m=700, B=1, H=8, W=6),      # long contraction: several pipeline periods and a tail
+    dict(m=2100, B=1, H=4, W=4),     # more input channels than the register kernel stages
+], ids=["m300", "m64", "m45", "m700", "m2100"])
+def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
+    """The bf16 pointwise kernels (1x1, N = 32, pixels per image a multiple of
+    4): the register-gathered kernel at each pipeline depth (reg2/4/6) and the
+    LDS-queue kernel at 1, 7 and the default number of workgroups.  Small
+    integers are exact in bf16 and in fp32 accumulation, so fp32 output is
+    bit-exact and bf16 output equals the oracle rounded to bf16.  Covers
+    ragged col-groups and a partial last set of 8 col-groups (n = 304), dense
+    to nearly empty col-groups (p = 0, 0.5, 0.97: for the queue kernel, steps
+    cut short where 16 kept channels span more chunks than LDS holds), and
+    workgroup counts that give each workgroup several work items."""
+    if variant.startswith("reg"):
+        monkeypatch.setenv("ONEXN_PWB_RP", variant[3:])
+    else:
+        monkeypatch.setenv("ONEXN_PWB_KERNEL", "queue")
+        if variant != "queue":
+            monkeypatch.setenv("ONEXN_PWB_WGS", variant[5:])
     c = shape
     n = 9 * 32 + 16
     w, x = workloads.gen_integer_layer(seed=c["m"] + int(c["B"]), cout=n, cin=c["m"], k=1,
                                        batch=c["B"], H=c["H"], W=c["W"], wmax=3, xmax=3)
-    print(f"pw bf16 {c} wgs={wgs}", flush=True)
+    print(f"pw bf16 {c} {variant}", flush=True)
     for p in (0.0, 0.5, 0.97):
         ref, _ = oracle_conv(w, x, 32, p, False, 1, 0)
         y, _ = gpu_conv(w.bfloat16(), x.bfloat16(), 32, p, False, 1, 0, "nchw", torch.float32)
