@@ -88,12 +88,15 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
         }
     }
 
-    const __amdgpu_buffer_rsrc_t rX =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.x), 0, int32_t(xbytes), kRawBufferFlags);
-    const __amdgpu_buffer_rsrc_t rD =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.D), 0, z1 * N * 4, kRawBufferFlags);
-    const __amdgpu_buffer_rsrc_t rI =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.I), 0, z1 * 4, kRawBufferFlags);
+    // The sizes are wave-uniform; saying so (readfirstlane) keeps the buffer
+    // resources in scalar registers -- a resource the compiler must treat as
+    // divergent turns every load into a loop over the distinct values.
+    const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(a.x), 0, __builtin_amdgcn_readfirstlane(int32_t(xbytes)), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rD = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(a.D), 0, __builtin_amdgcn_readfirstlane(z1 * N * 4), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(z1 * 4), kRawBufferFlags);
     const uint32_t chb = uint32_t(a.x_c) * 4;   // bytes between input channels
 
     acc_t acc[NB];
