@@ -134,25 +134,39 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
         if (wave == 0)
             copy4_to_lds(rI, (const lds_char*)(sI + (c % 3) * 64), (zb + c * CC + lane) * 4, 0);
     };
-    // Stages chunk c: its weight blocks and its channels' input rows.
+    // Stages chunk c: its weight blocks and its channels' input rows.  The
+    // copies are issued straight-line per staged position block k (one
+    // uniform test per k, selects rather than branches for the channels), so
+    // a chunk's staging costs few instructions besides the copies themselves.
     auto stage = [&](int32_t c, int buf) {
         const lds_char* dd = (const lds_char*)(ds + buf * DBUF);
         const int32_t d0 = (zb + c * CC) * (N * KK * 4);
-        for (int32_t e0 = wave * 64; e0 < DBUF; e0 += kKxThreads)
-            copy4_to_lds(rD, dd + e0 * 4, d0 + (e0 + lane) * 4, 0);
+        if constexpr (DBUF % (4 * kKxThreads) == 0) {   // 16-byte copies: blocks are whole 16-byte pieces
+            for (int32_t e0 = wave * 256; e0 < DBUF; e0 += 4 * kKxThreads)
+                copy16_to_lds(rD, dd + e0 * 4, d0 + (e0 + 4 * lane) * 4, 0);
+        } else {
+            for (int32_t e0 = wave * 64; e0 < DBUF; e0 += kKxThreads)
+                copy4_to_lds(rD, dd + e0 * 4, d0 + (e0 + lane) * 4, 0);
+        }
         // Lane j < CC: block j's channel, or -1 past the col-group's end.
         const int32_t chv = (lane < CC && zb + c * CC + lane < ze) ? sI[(c % 3) * 64 + lane] : -1;
         const lds_char* xd = (const lds_char*)(xs + buf * XBUF);
+        // An invalid position or channel carries kBufferOutOfRange: the sum of
+        // two offsets below 2^31 stays below 2^32 and an out-of-range one
+        // keeps the sum at or above kBufferOutOfRange, past every buffer.
+        uint32_t choff[CC];
 #pragma unroll
         for (int j = 0; j < CC; ++j) {
             const int32_t ch = __builtin_amdgcn_readlane(chv, j);
-            const uint32_t choff = (ch >= 0 && ch < a.m) ? uint32_t(ch) * uint32_t(a.x_c) * 4u : kBufferOutOfRange;
+            choff[j] = uint32_t(ch) < uint32_t(a.m) ? uint32_t(ch) * uint32_t(a.x_c) * 4u : kBufferOutOfRange;
+        }
 #pragma unroll
-            for (int k = 0; k < kKxMaxRem; ++k) {
-                const int32_t rem0 = wave * 64 + k * kKxThreads;
-                if (rem0 < VRWp)
-                    copy4_to_lds(rX, xd + (j * CP + rem0) * 4, int32_t(min(spk[k] + choff, kBufferOutOfRange)), 0);
-            }
+        for (int k = 0; k < kKxMaxRem; ++k) {
+            const int32_t rem0 = wave * 64 + k * kKxThreads;
+            if (rem0 >= VRWp) break;
+#pragma unroll
+            for (int j = 0; j < CC; ++j)
+                copy4_to_lds(rX, xd + (j * CP + rem0) * 4, int32_t(spk[k] + choff[j]), 0);
         }
     };
 
