@@ -39,9 +39,9 @@ namespace onexn {
 namespace {
 
 constexpr int kDThreads = 256;
-constexpr int kDB = 8;   // MFMA steps per batch
-
-template <int N, int NB, int KSPLIT>
+// kDB: MFMA steps per batch (8 for long contractions, 2 for short ones,
+// whose waves would otherwise multiply mostly zero padding).
+template <int N, int NB, int KSPLIT, int kDB>
 __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
@@ -76,7 +76,7 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int32_t p = (pb * NB + nb) * COLS + col;
-        xo[nb] = xbytes;
+        xo[nb] = kBufferOutOfRange;
         yo[nb] = -1;
         if (live && p < a.npix) {
             const int32_t b = p / a.HWo, hw = p - b * a.HWo;
@@ -105,56 +105,66 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) acc[nb][r] = 0.f;
 
-    struct Batch {
-        float av[kDB];
-        float bv[kDB][NB];
-    };
-    // Channel indices come in windows of 64 entries (lane j: entry wbase + j),
-    // loaded a window ahead of use, so a batch's input addresses never wait
-    // for an index load.  Entries at or past z1 and channels outside [0, m)
-    // read zeros.
-    constexpr int E = kDB * KS;   // entries per batch (divides 64)
-    static_assert(64 % E == 0, "batches tile the index windows");
+    // A batch is kDB steps = E entries.  Its channel indices (lane j: entry
+    // z + j) are loaded two batches ahead and turned into the byte offset of
+    // each entry's input channel -- kBufferOutOfRange for an entry at or past
+    // z1 or a channel outside [0, m), which reads zeros.  A step then costs
+    // one lane shuffle of that offset and one add per column block besides
+    // its loads: the matrix pipe of a SIMD idles while other waves issue, so
+    // every instruction per MFMA counts.  The two batches in flight live in
+    // register slots with compile-time indices and the loop body is
+    // straight-line (scheduling barriers keep each batch's loads in order);
+    // otherwise the compiler copies batches and accumulators between
+    // registers on every trip and waits for all loads at the loop head.
+    constexpr int E = kDB * KS;   // entries per batch
+    static_assert(E <= 64, "a batch's indices fit one wave");
+    float av[2][kDB], bv[2][kDB][NB];
+    int32_t idx[2];
     auto load_idx = [&](int32_t z) { return int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, (z + lane) * 4, 0, 0)); };
-    int32_t wbase = z0;
-    int32_t ivw = load_idx(z0), ivn = load_idx(z0 + 64);
-    auto issue = [&](Batch& bt, int32_t z) {
-        if (z - wbase >= 64) {
-            wbase += 64;
-            ivw = ivn;
-            ivn = load_idx(wbase + 64);
-        }
-        const int32_t off = z - wbase;
+    auto issue = [&](int sl, int32_t z) __attribute__((always_inline)) {
+        const bool ok = (z + lane < z1) & (uint32_t(idx[sl]) < uint32_t(a.m));
+        const uint32_t cw = ok ? uint32_t(idx[sl]) * chb : kBufferOutOfRange;
+        idx[sl] = load_idx(z + 2 * E);
+        uint32_t co[kDB];
+#pragma unroll
+        for (int st = 0; st < kDB; ++st)
+            co[st] = uint32_t(__builtin_amdgcn_ds_bpermute(4 * (st * KS + kk), int32_t(cw)));
 #pragma unroll
         for (int st = 0; st < kDB; ++st) {
-            const int32_t ze_ = z + st * KS;
-            bt.av[st] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rD, (ze_ * N + lane) * 4, 0, 0));
-            const int32_t ch = __builtin_amdgcn_ds_bpermute(4 * (off + st * KS + kk), ivw);
-            const bool ok = ze_ + kk < z1 && uint32_t(ch) < uint32_t(a.m);
-            const uint32_t choff = ok ? uint32_t(ch) * chb : xbytes;
+            av[sl][st] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                rD, ((z + st * KS) * N + lane) * 4, 0, 0));
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                bt.bv[st][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                    rX, int32_t(min(xo[nb] + choff, xbytes)), 0, 0));
+            for (int nb = 0; nb < NB; ++nb)   // both terms below 2^31: no wrap, out of range stays out
+                bv[sl][st][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rX, int32_t(xo[nb] + co[st]), 0, 0));
         }
     };
-    auto consume = [&](const Batch& bt) {
+    auto consume = [&](int sl) __attribute__((always_inline)) {
 #pragma unroll
         for (int st = 0; st < kDB; ++st)
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) acc[nb] = M::step(bt.av[st], bt.bv[st][nb], acc[nb]);
+            for (int nb = 0; nb < NB; ++nb) acc[nb] = M::step(av[sl][st], bv[sl][st][nb], acc[nb]);
     };
 
+    // Batches in pairs, each issued one batch ahead of its MFMAs.  An odd
+    // count runs one batch of zeros (past the end everything reads zero): a
+    // separate tail would merge with the loop body and bring the copies back.
     const int32_t nbat = (z1 - z0 + E - 1) / E;
     if (nbat > 0) {
-        Batch b0, b1;
-        issue(b0, z0);
-        for (int32_t bi = 0; bi < nbat; bi += 2) {
-            if (bi + 1 < nbat) issue(b1, z0 + (bi + 1) * E);
-            consume(b0);
-            if (bi + 1 >= nbat) break;
-            if (bi + 2 < nbat) issue(b0, z0 + (bi + 2) * E);
-            consume(b1);
+        idx[0] = load_idx(z0);
+        idx[1] = load_idx(z0 + E);
+        issue(0, z0);
+        const int32_t npair = (nbat + 1) >> 1;
+        for (int32_t pi = 0; pi < npair; ++pi) {
+            const int32_t z = z0 + 2 * pi * E;
+            __builtin_amdgcn_sched_barrier(0);
+            issue(1, z + E);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(0);
+            __builtin_amdgcn_sched_barrier(0);
+            issue(0, z + 2 * E);
+            __builtin_amdgcn_sched_barrier(0);
+            consume(1);
         }
     }
 
@@ -188,10 +198,17 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
 
 template <int N, int NB, int KSPLIT>
 onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
-    constexpr int COLS = PwMfma<N>::COLS;
+    constexpr int COLS = PwMfma<N>::COLS, KS = PwMfma<N>::KS;
     const int64_t units = (int64_t(a.npix) + NB * COLS - 1) / (NB * COLS) * a.G;
     const int64_t upw = 4 / KSPLIT;
-    return launch_grid(pw_direct<N, NB, KSPLIT>, a, (units + upw - 1) / upw, s, kDThreads);
+    const int64_t grid = (units + upw - 1) / upw;
+    // A wave's entries run in whole pairs of batches: short shares take
+    // small batches.
+    const int64_t per_wave = a.G > 0 ? a.t / a.G / KSPLIT : 0;
+    int kdb = per_wave < 8 * 8 * KS ? 2 : 8;
+    if (const char* env = std::getenv("ONEXN_DIRECT_KDB")) kdb = std::atoi(env);   // testing
+    if (kdb == 2) return launch_grid(pw_direct<N, NB, KSPLIT, 2>, a, grid, s, kDThreads);
+    return launch_grid(pw_direct<N, NB, KSPLIT, 8>, a, grid, s, kDThreads);
 }
 
 // (column blocks per unit, waves per unit): the largest tile that gives every

@@ -461,6 +461,7 @@ def test_pw_fma_integer_exact(case, tile, monkeypatch):
         np.testing.assert_array_equal(y, ref)
 
 
+@pytest.mark.parametrize("kdb", ["2", "8"])
 @pytest.mark.parametrize("tile", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("case", [
     dict(N=32, m=45, n=80, B=3, H=28, W=28, s=2, pd=0),   # strided 1x1 (downsample)
@@ -468,16 +469,19 @@ def test_pw_fma_integer_exact(case, tile, monkeypatch):
     dict(N=32, m=700, n=40, B=2, H=7, W=7, s=1, pd=0),    # long contraction, few pixels
     dict(N=16, m=33, n=20, B=1, H=10, W=13, s=3, pd=2),
 ], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
-def test_pw_direct_integer_exact(case, tile, monkeypatch):
+def test_pw_direct_integer_exact(case, tile, kdb, monkeypatch):
     """The 1x1 kernel with register-loaded operands at every tile shape
-    (column blocks per unit, waves splitting the contraction): strides,
-    padding, ragged col-groups and pixel tails, p from dense to nearly empty."""
+    (column blocks per unit, waves splitting the contraction) and both batch
+    sizes (2 and 8 MFMA steps; odd batch counts run a batch of zeros):
+    strides, padding, ragged col-groups and pixel tails, p from dense to
+    nearly empty."""
     monkeypatch.setenv("ONEXN_DIRECT_TILE", tile)
+    monkeypatch.setenv("ONEXN_DIRECT_KDB", kdb)
     monkeypatch.setenv("ONEXN_PW_KERNEL", "direct")
     c = case
     w, x = workloads.gen_integer_layer(seed=c["m"] + c["n"], cout=c["n"], cin=c["m"], k=1,
                                        batch=c["B"], H=c["H"], W=c["W"], wmax=1, xmax=2)
-    print(f"pw direct {c} tile={tile}", flush=True)
+    print(f"pw direct {c} tile={tile} kdb={kdb}", flush=True)
     for p in (0.0, 0.5, 0.95):
         y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
         ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
