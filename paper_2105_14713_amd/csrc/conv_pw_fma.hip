@@ -247,7 +247,11 @@ onexn_status launch_n(ConvArgs a, hipStream_t s) {
     int choice = 0;
     if (const char* env = std::getenv("ONEXN_FMA_TILE")) choice = std::atoi(env);   // testing
     if (choice == 0) {
-        if (tiles(256) * gs4 >= want) choice = 1;
+        // The widest tile also wins with fewer workgroups (down to ~1.5 per
+        // compute unit) unless the col-groups are long (measured on the
+        // MobileNet-V2 pointwise layers at N = 4 and 8).
+        if (tiles(256) * gs4 >= want || (2 * tiles(256) * gs4 >= 3 * int64_t(device_cu_count()) && avg_kept < 400))
+            choice = 1;
         else if (tiles(128) * gs4 >= want) choice = 2;
         else if (tiles(64) * gs4 >= want || avg_kept < 64) choice = 3;
         else if (tiles(64) * gs2 >= want || avg_kept < 128) choice = 4;
