@@ -80,7 +80,7 @@ template <typename TY, int kRP>
 __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     constexpr int kRSlots = kRP + 1;   // register slots of the pipeline
     __shared__ __attribute__((aligned(16))) char sA[kRWaves * 1024];
-    __shared__ __attribute__((aligned(16))) int32_t sI[kRWaves * kRWin];
+    __shared__ __attribute__((aligned(16))) int32_t sI[kRWaves * (kRWin + 16)];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     const bool gvalid = gi < batch * gpi;
     const int32_t b = gvalid ? gi / gpi : 0, jg = gvalid ? gi - b * gpi : 0;
     const int32_t xbytes = int32_t(int64_t(batch) * a.x_img * 2);
-    const uint32_t pixoff = uint32_t((int64_t(b) * a.x_img + 4 * jg) * 2);
+    const uint32_t pixoff = gvalid ? uint32_t((int64_t(b) * a.x_img + 4 * jg) * 2) : kBufferOutOfRange;
     const uint32_t chb = uint32_t(a.HWo) * 2;   // bytes between input channels
 
     const __amdgpu_buffer_rsrc_t rX =
@@ -119,30 +119,37 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     // staged in the wave's LDS once and read back as 8 consecutive entries
     // per lane, so index reads use the LDS counter and never wait behind
     // input loads.  Entries past the col-group read zeros.
-    int32_t* const win = sI + wave * kRWin;
+    // Each staged index is then turned, once, into the byte offset of its
+    // input row (kBufferOutOfRange for a channel outside [0, m) and for the
+    // 16 entries past the col-group's end), so a gathered load costs one add.
+    int32_t* const win = sI + wave * (kRWin + 16);
     {
         const v4i32 rIw = buffer_rsrc(a.I, ze * 4);
         const int32_t nE = ze - zb;
         for (int32_t e = 0; e < nE; e += 64)
             copy4_to_lds(rIw, (const lds_char*)(win + e), (zb + e + lane) * 4, 0);
         vm_wait<0>();
+        for (int32_t e = lane; e < nE + 16; e += 64) {
+            const int32_t ch = e < nE ? win[e] : -1;
+            win[e] = int32_t(uint32_t(ch) < uint32_t(a.m) ? uint32_t(ch) * chb : kBufferOutOfRange);
+        }
     }
 
     // Pipeline registers, indexed by step % kRSlots.
     u32x2 xv[kRSlots][8];    // the lane's granule at the channels of entries 8 h .. 8 h + 7
     i32x4 av[kRSlots];       // the lane's 16 bytes of the step's weights
 
+    // Steps past the last one (only ever prefetched, never multiplied) read
+    // clamped window positions: any offset is safe in a range-checked load.
     auto load_step = [&](int s, int32_t step) __attribute__((always_inline)) {
-        const int32_t e0 = zb + step * 16 + 8 * h;
-        const int32_t rel = min(step * 16 + 8 * h, kRWin - 8);
+        const int32_t rel = min(step * 16 + 8 * h, kRWin + 8);
         const i32x4 c03 = *reinterpret_cast<const i32x4*>(win + rel);
         const i32x4 c47 = *reinterpret_cast<const i32x4*>(win + rel + 4);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int32_t ch = j < 4 ? c03[j] : c47[j - 4];
-            const uint32_t addr = pixoff + uint32_t(ch) * chb;
-            const bool ok = gvalid & (e0 + j < ze) & (uint32_t(ch) < uint32_t(a.m));
-            const uint32_t off = ok ? addr : kBufferOutOfRange;
+            // Both terms are below 2^31, and either one out of range keeps
+            // the sum out of range (no wrap).
+            const uint32_t off = pixoff + uint32_t(j < 4 ? c03[j] : c47[j - 4]);
             xv[s][j] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rX, int32_t(off), 0, 0));
         }
         av[s] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(
