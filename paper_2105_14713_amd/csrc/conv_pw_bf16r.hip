@@ -13,24 +13,24 @@
 // entries 8 h .. 8 h + 7 of one row (A: output q) or one column (B: pixel q).
 //
 // B without a transposition buffer.  A wave computes one col-group over a
-// tile of 128 pixels: 32 granules of 4 consecutive pixels of one image (the
-// pixels of an image are a multiple of 4), lane q owning granule q.  For a
-// step of 16 kept blocks, lane (h, q) loads its granule from the 8 input rows
-// of entries 8 h .. 8 h + 7 (8 bytes each), i.e. an 8 x 4 block of bf16
-// values; byte permutes regroup it into four B fragments, one per pixel of
-// the granule, so MFMA column block k is pixel 4 q + k.  Each load reads 256
-// contiguous bytes per half-wave.  A lane's four outputs of a row are
-// consecutive pixels again, stored with one 8- or 16-byte write.
+// tile of 32 granules of GP = 8 (or 4) consecutive pixels of one image, lane
+// q owning granule q.  For a step of 16 kept blocks, lane (h, q) loads its
+// granule from the 8 input rows of entries 8 h .. 8 h + 7 (16 or 8 bytes
+// each), i.e. an 8 x GP block of bf16 values; byte permutes regroup it into
+// GP B fragments, one per pixel of the granule, so MFMA column block k is
+// pixel k of granule q.  Each load reads 512 (256) contiguous bytes per
+// half-wave.  A lane's outputs of a row are consecutive pixels again, stored
+// with 8- or 16-byte writes.
 //
 // A fragments.  A step's 16 blocks of D are one contiguous kilobyte
 // (16 x 32 bf16, output-contiguous); a lane loads 16 bytes of it, writes them
 // to the wave's LDS slot, and two ds_read_b64_tr_b16 transpose the slot into
 // the A fragment (lane (h, q) reads entries 8 h + i of output q).
 //
-// Pipelining.  The loads of step j + kRP (inputs and weights) and the
-// channel indices of step j + 2 kRP are issued before the MFMAs of step j,
-// so every load has kRP steps of other waves' and its own work to land.  All
-// waits are the compiler's own vmcnt counts over these builtin loads.
+// Pipelining.  The loads of step j + kRP (inputs and weights) are issued
+// before the MFMAs of step j, so every load has kRP steps of other waves' and
+// its own work to land.  All waits are the compiler's own vmcnt counts over
+// these builtin loads; the channel indices come from LDS.
 // Entries past the col-group's end, and channels outside [0, m), load zero
 // inputs (an out-of-range buffer offset) and zero weights (the weight buffer
 // ends at the col-group's last block), so they add exactly nothing.
@@ -39,6 +39,7 @@
 // tile; the workgroups of a tile are consecutive, so they run on one XCD and
 // share the tile's input rows in its L2.
 #include <cstdlib>
+#include <type_traits>
 
 #include "lds_copy.h"
 #include "pw_common.h"
@@ -60,6 +61,7 @@ __device__ __forceinline__ v4i16 tr_read(const lds_char* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p);
 }
 
+// A lane's outputs of one row: 4 (or the upper 4 of 8) consecutive pixels.
 template <typename TY> struct Out4;
 template <> struct Out4<uint16_t> {
     typedef u32x2 T;   // four bf16
@@ -75,9 +77,16 @@ template <> struct Out4<float> {
     __device__ static T pack(float a, float b, float c, float d) { return T{a, b, c, d}; }
 };
 
-// kRP: steps of loads in flight ahead of the multiplied step.
-template <typename TY, int kRP>
+// kRP: steps of loads in flight ahead of the multiplied step.  GP: pixels
+// per granule (4: 8-byte loads, a 128-pixel tile; 8: 16-byte loads, a
+// 256-pixel tile, fewer cache lines per gathered byte and half the weight
+// reads per MFMA; an image's last granule then starts 8 pixels before its
+// end and its first pixels, duplicates of the previous granule's, are not
+// stored).
+template <typename TY, int kRP, int GP>
 __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
+    static_assert(GP == 4 || GP == 8, "granule of 4 or 8 pixels");
+    typedef typename std::conditional<GP == 8, u32x4, u32x2>::type gran_t;
     constexpr int kRSlots = kRP + 1;   // register slots of the pipeline
     __shared__ __attribute__((aligned(16))) char sA[kRWaves * 1024];
     __shared__ __attribute__((aligned(16))) int32_t sI[kRWaves * (kRWin + 16)];
@@ -93,14 +102,16 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     if (g < a.G) group_range(a, g, zb, ze);
     const int32_t nsteps = (ze - zb + 15) >> 4;
 
-    // The lane's granule: image b, pixels 4 jg .. 4 jg + 3.
+    // The lane's granule: image b, pixels hw0 .. hw0 + GP - 1, of which the
+    // first `dup` repeat the previous granule's (an image's last granule).
     const int32_t batch = a.npix / a.HWo;
-    const int32_t gpi = a.HWo >> 2;
+    const int32_t gpi = (a.HWo + GP - 1) / GP;
     const int32_t gi = tile * kRGran + q;
     const bool gvalid = gi < batch * gpi;
     const int32_t b = gvalid ? gi / gpi : 0, jg = gvalid ? gi - b * gpi : 0;
+    const int32_t hw0 = min(GP * jg, a.HWo - GP), dup = GP * jg - hw0;
     const int32_t xbytes = int32_t(int64_t(batch) * a.x_img * 2);
-    const uint32_t pixoff = gvalid ? uint32_t((int64_t(b) * a.x_img + 4 * jg) * 2) : kBufferOutOfRange;
+    const uint32_t pixoff = gvalid ? uint32_t((int64_t(b) * a.x_img + hw0) * 2) : kBufferOutOfRange;
     const uint32_t chb = uint32_t(a.HWo) * 2;   // bytes between input channels
 
     const __amdgpu_buffer_rsrc_t rX =
@@ -136,7 +147,7 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     }
 
     // Pipeline registers, indexed by step % kRSlots.
-    u32x2 xv[kRSlots][8];    // the lane's granule at the channels of entries 8 h .. 8 h + 7
+    gran_t xv[kRSlots][8];   // the lane's granule at the channels of entries 8 h .. 8 h + 7
     i32x4 av[kRSlots];       // the lane's 16 bytes of the step's weights
 
     // Steps past the last one (only ever prefetched, never multiplied) read
@@ -150,15 +161,18 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
             // Both terms are below 2^31, and either one out of range keeps
             // the sum out of range (no wrap).
             const uint32_t off = pixoff + uint32_t(j < 4 ? c03[j] : c47[j - 4]);
-            xv[s][j] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rX, int32_t(off), 0, 0));
+            if constexpr (GP == 8)
+                xv[s][j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rX, int32_t(off), 0, 0));
+            else
+                xv[s][j] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rX, int32_t(off), 0, 0));
         }
         av[s] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                               rD, (zb + step * 16) * 64 + lane * 16, 0, 0));
     };
 
-    f32x16 acc[4];
+    f32x16 acc[GP];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
+    for (int k = 0; k < GP; ++k)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[k][r] = 0.f;
 
@@ -170,7 +184,7 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
         const bf16x8 af = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         // B: fragment k takes pixel k of the granule from each of the 8 rows.
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int k = 0; k < GP; ++k) {
             const uint32_t sel = (k & 1) ? 0x07060302u : 0x05040100u;
             u32x4 bw;
 #pragma unroll
@@ -202,32 +216,48 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     for (int u = 0; u < kRSlots - 1; ++u)
         if (nfull + u < nsteps) step(u, nfull + u);
 
-    // Store: MFMA (row, col) of block k -> output channel g*32 + row, pixel 4 col + k of the tile.
+    // Store: MFMA (row, col) of block k -> output channel g*32 + row, pixel
+    // hw0 + k of the lane's granule (col), k >= dup.
     if (g >= a.G || !gvalid) return;
     TY* __restrict__ y = static_cast<TY*>(a.y);
-    TY* const yb = y + int64_t(b) * a.y_img + 4 * jg;
+    TY* const yb = y + int64_t(b) * a.y_img + hw0;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int32_t o = g * 32 + PwMfma<32>::row(lane, r);
-        if (o < a.n)
-            *reinterpret_cast<typename Out4<TY>::T*>(yb + int64_t(o) * a.y_c) =
-                Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+        if (o >= a.n) continue;
+        TY* const yr = yb + int64_t(o) * a.y_c;
+        if constexpr (GP == 8) {
+            if (dup == 0)
+                *reinterpret_cast<typename Out4<TY>::T*>(yr) = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+            *reinterpret_cast<typename Out4<TY>::T*>(yr + 4) = Out4<TY>::pack(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
+        } else {
+            *reinterpret_cast<typename Out4<TY>::T*>(yr) = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+        }
     }
 }
 
 template <typename TY>
 onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     const int64_t batch = a.npix / a.HWo;
-    const int64_t tiles = (batch * (a.HWo / 4) + kRGran - 1) / kRGran;
     const int64_t gsets = (a.G + kRWaves - 1) / kRWaves;
-    // Two steps in flight measured fastest on the 2048 -> 2048 layer (deeper
-    // pipelines add register pressure without more bandwidth).
-    int rp = 2;
+    // 8-pixel granules where an image has at least 8 pixels (2048 -> 2048 at
+    // 14x14: 380 us against 445 us with 4-pixel ones, from fewer cache lines
+    // per gathered byte), else 4.  Steps in flight: one for 8-pixel granules
+    // (their accumulators take twice the registers), two for 4 (deeper
+    // pipelines add registers, not bandwidth).
+    int gp = a.HWo >= 8 ? 8 : 4, rp = 0;
+    if (const char* env = std::getenv("ONEXN_PWB_GP")) gp = std::atoi(env);   // testing
     if (const char* env = std::getenv("ONEXN_PWB_RP")) rp = std::atoi(env);   // testing
+    if (gp == 8 && a.HWo >= 8) {
+        const int64_t grid = (batch * ((a.HWo + 7) / 8) + kRGran - 1) / kRGran * gsets;
+        if (rp == 2) return launch_grid(pw_bf16r<TY, 2, 8>, a, grid, s, kRThreads);
+        return launch_grid(pw_bf16r<TY, 1, 8>, a, grid, s, kRThreads);
+    }
+    const int64_t grid = (batch * (a.HWo / 4) + kRGran - 1) / kRGran * gsets;
     switch (rp) {
-        case 4: return launch_grid(pw_bf16r<TY, 4>, a, tiles * gsets, s, kRThreads);
-        case 6: return launch_grid(pw_bf16r<TY, 6>, a, tiles * gsets, s, kRThreads);
-        default: return launch_grid(pw_bf16r<TY, 2>, a, tiles * gsets, s, kRThreads);
+        case 4: return launch_grid(pw_bf16r<TY, 4, 4>, a, grid, s, kRThreads);
+        case 6: return launch_grid(pw_bf16r<TY, 6, 4>, a, grid, s, kRThreads);
+        default: return launch_grid(pw_bf16r<TY, 2, 4>, a, grid, s, kRThreads);
     }
 }
 

@@ -332,7 +332,7 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
         np.testing.assert_array_equal(y, ref)
 
 
-@pytest.mark.parametrize("variant", ["reg2", "reg4", "reg6", "queue1", "queue7", "queue"])
+@pytest.mark.parametrize("variant", ["g4rp2", "g4rp4", "g4rp6", "g8rp1", "g8rp2", "queue1", "queue7", "queue"])
 @pytest.mark.parametrize("shape", [
     dict(m=300, B=3, H=14, W=14),    # 5 channel chunks (ragged last), partial last granule per image
     dict(m=64, B=2, H=12, W=12),     # one chunk, whole granules, tiles across images
@@ -342,16 +342,19 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
 ], ids=["m300", "m64", "m45", "m700", "m2100"])
 def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
     """The bf16 pointwise kernels (1x1, N = 32, pixels per image a multiple of
-    4): the register-gathered kernel at each pipeline depth (reg2/4/6) and the
-    LDS-queue kernel at 1, 7 and the default number of workgroups.  Small
+    4): the register-gathered kernel with 4-pixel granules at pipeline depths
+    2, 4, 6 and with 8-pixel granules at depths 1, 2 (images of 12 and 196
+    pixels end in a half-duplicate granule), and the LDS-queue kernel at 1, 7
+    and the default number of workgroups.  Small
     integers are exact in bf16 and in fp32 accumulation, so fp32 output is
     bit-exact and bf16 output equals the oracle rounded to bf16.  Covers
     ragged col-groups and a partial last set of 8 col-groups (n = 304), dense
     to nearly empty col-groups (p = 0, 0.5, 0.97: for the queue kernel, steps
     cut short where 16 kept channels span more chunks than LDS holds), and
     workgroup counts that give each workgroup several work items."""
-    if variant.startswith("reg"):
-        monkeypatch.setenv("ONEXN_PWB_RP", variant[3:])
+    if variant.startswith("g"):
+        monkeypatch.setenv("ONEXN_PWB_GP", variant[1])
+        monkeypatch.setenv("ONEXN_PWB_RP", variant[4:])
     else:
         monkeypatch.setenv("ONEXN_PWB_KERNEL", "queue")
         if variant != "queue":
