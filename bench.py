@@ -129,7 +129,17 @@ def cpu_baseline(layers, batch, wl, budget_s):
             spent += time.perf_counter() - t0
             done_f += 2.0 * layer.Ho * layer.Ho * layer.N * layer.k * layer.k * pr.t
         imgs += 1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": done_f / spent / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "cpu_model": cpu_model, "host_cpus": os.cpu_count(),
             "kind": "oracle",
             "sample": f"{imgs} single-image passes (the workload has batch {batch}) through all "
                       f"{len(layers)} layer(s): fp64 direct convolution over the masked dense "
