@@ -299,11 +299,11 @@ KxShape kx_shape(const ConvArgs& a, int tp, int cc) {
     return s;
 }
 
-int kx_cc(int N, int k) { return k == 7 ? (N == 32 ? 2 : 4) : 8; }
+int kx_cc(int N, int k) { return k == 7 ? (N == 32 ? 2 : 4) : 4; }
 
 template <int N, int K, int NBW>
 onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
-    constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : 8;
+    constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : 4;
     a.kx_rows = s.rows;
     a.kx_wp = s.wp;
     a.kx_vrwp = s.vrwp;
