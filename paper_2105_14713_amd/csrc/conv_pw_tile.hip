@@ -52,6 +52,7 @@ constexpr int kTileBufFloats = 16384;                   // one X tile buffer: 64
 constexpr int kTileSteps = 4;                           // MFMA steps per block
 constexpr int kTileMaxG = 256;                          // col-groups a layer may have
 constexpr int32_t kBufferFlags = 0x00020000;            // buffer resource word 3: 32-bit raw data
+constexpr int kTileEarly = 32;                          // copies of the second tile issued before the first is awaited
 
 __device__ __forceinline__ int32_t lds_load(const int32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -116,22 +117,42 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
         else
             __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
     };
-    auto copy_tile = [&](int32_t T, int b) {
+    // `early` (copy of the second tile while the first is in flight): once
+    // kTileEarly of its loads are issued, every load of the first tile has
+    // completed (loads complete in issue order), so the first tile is
+    // published as landed there.  Returns whether that happened.
+    auto land_first = [&]() {
+        if (lane == 0) lds_store(&sLanded[0], 1);
+    };
+    auto copy_tile = [&](int32_t T, int b, bool early) {
         float* dst0 = sX + b * kTileBufFloats;
+        int32_t issued = 0;
+        auto count = [&]() {
+            if (early && ++issued == kTileEarly) {
+                wait_vmem<kTileEarly>();
+                land_first();
+            }
+        };
         if (spr <= 64) {
             const int32_t rpl = 64 >> spr_shift;           // rows per load
             const int32_t row0 = lane >> spr_shift;
             const float* src = pixel_src(T, lane & (spr - 1)) + int64_t(row0) * a.x_c;
             const int64_t step = int64_t(rpl) * a.x_c;
-            for (int32_t j = 0; j * rpl < a.m; ++j, src += step)
+            for (int32_t j = 0; j * rpl < a.m; ++j, src += step) {
                 if (j * rpl + row0 < a.m) dma(src, dst0 + j * 64 * EB);
+                count();
+            }
         } else {
             const int32_t nb = spr >> 6;
             for (int32_t pb = 0; pb < nb; ++pb) {
                 const float* src = pixel_src(T, 64 * pb + lane);
-                for (int32_t r = 0; r < a.m; ++r, src += a.x_c) dma(src, dst0 + (r * nb + pb) * 64 * EB);
+                for (int32_t r = 0; r < a.m; ++r, src += a.x_c) {
+                    dma(src, dst0 + (r * nb + pb) * 64 * EB);
+                    count();
+                }
             }
         }
+        return issued >= kTileEarly;
     };
 
     const bool loader = wave == kTileCompute;
@@ -151,7 +172,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     // meet on an LDS counter, not a barrier, so that none of them waits for
     // the loader to finish issuing the copy.
     if (loader) {
-        copy_tile(Tfirst, 0);
+        copy_tile(Tfirst, 0, false);
     } else {
         for (int32_t c = wave; c * 16 <= G; c += kTileCompute) {
             int32_t v = 0;
@@ -209,6 +230,11 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     }
 
     if (loader) {
+        // A range whose first tile has few units (fewer than a.tile_early)
+        // copies its second tile right behind the first instead of after
+        // it: the waves the first tile cannot keep busy would otherwise idle
+        // for a whole copy.
+        const bool early = ntiles > 1 && unit_end(0) - unit_begin(0) < a.tile_early;
         for (int32_t k = 0; k < ntiles; ++k) {
             const int b = k & 1;
             if (k >= 2) {
@@ -219,12 +245,18 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
             // The units can be handed out before the tile lands: compute
             // waves load their first blocks' weights and indices meanwhile.
             // (The first tile's counter is set by compute wave 0.)
-            if (k > 0) {
+            if (k > 0 && !(k == 1 && early)) {
                 if (lane == 0) lds_store(&sNext[b], unit_begin(k));
                 wait_lgkm();
                 if (lane == 0) lds_store(&sReady[b], k + 1);
             }
-            if (k > 0 || Tfirst != T0) copy_tile(T0 + k, b);
+            if ((k > 0 && !(k == 1 && early)) || (k == 0 && Tfirst != T0)) copy_tile(T0 + k, b, false);
+            if (k == 0 && early) {
+                if (lane == 0) lds_store(&sNext[1], unit_begin(1));
+                wait_lgkm();
+                if (lane == 0) lds_store(&sReady[1], 2);
+                if (copy_tile(T0 + 1, 1, true)) continue;   // the first tile is published
+            }
             wait_vmem<0>();   // the tile has landed in LDS
             if (lane == 0) lds_store(&sLanded[b], k + 1);
         }
@@ -496,6 +528,8 @@ onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
     const int64_t total = tiles * a.slices * (int64_t(a.t) + a.G);
     a.cost_q = int32_t(total / wgs);
     a.cost_r = int32_t(total % wgs);
+    a.tile_early = 2 * kTileCompute;
+    if (const char* env = std::getenv("ONEXN_TILE_EARLY")) a.tile_early = std::atoi(env);
     if (vec4_ok(a)) return launch_grid(pw_tile_f32<N, SW, true>, a, wgs, s, kTileThreads);
     return launch_grid(pw_tile_f32<N, SW, false>, a, wgs, s, kTileThreads);
 }
