@@ -36,8 +36,7 @@ struct ConvArgs {
     int32_t total;      // workgroups in the grid
     int32_t tile_ranges;   // streamed pointwise kernel: pixel-tile ranges per col-group set
     int32_t slices;        // resident-tile pointwise kernel: slices per pixel tile,
-    int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder),
-    int32_t tile_early;       // and the first-tile unit count below which the second tile is copied at once
+    int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder)
     int32_t kx_rows;       // k x k staged kernel: output rows per tile,
     int32_t kx_wp, kx_vrwp, kx_cp;   // staged row width, input rows x row width, channel pitch (floats)
 };

@@ -96,6 +96,10 @@ __global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
     const int32_t nel = nt * nch;   // X stream: element e = chunk e % nch of tile tile0 + e / nch
 
     if (wave == kPwWaves) {
+        // (Issue arbitration favours older waves; the loader, the youngest,
+        // gets the highest priority so that its copies are not issued only
+        // in the compute waves' gaps.)
+        __builtin_amdgcn_s_setprio(3);
         // Loader wave.  Element e goes to ring buffer e % kPwRing.  Load j
         // covers LDS floats [j*64*EB, (j+1)*64*EB) of the buffer
         // (lane-contiguous, as loads into LDS require): lane slot f = j*64 +

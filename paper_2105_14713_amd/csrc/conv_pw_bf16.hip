@@ -133,6 +133,10 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
     const lds_char* const lx = (const lds_char*)sX;
 
     if (wave >= kQWaves) {
+        // (Issue arbitration favours older waves; the loaders, the youngest,
+        // get the highest priority so that their copies are not issued only
+        // in the compute waves' gaps.)
+        __builtin_amdgcn_s_setprio(3);
         // ---- Loader waves.  Chunk sequence number s = k * nchunks + c (the
         // workgroup's item k, channel chunk c) goes to buffer s % kQRing;
         // loader wave l copies the chunks with s % kQLoaders == l, up to
