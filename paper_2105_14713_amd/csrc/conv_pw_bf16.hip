@@ -393,7 +393,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int32_t o = g * 32 + PwMfma<32>::row(lane, r);
-                    if (o < a.n) yb[int64_t(o) * a.y_c] = from_f32<TY>(acc[e][r]);
+                    if (o < a.n) store_out(&yb[int64_t(o) * a.y_c], from_f32<TY>(acc[e][r]));
                 }
             }
         }

@@ -76,6 +76,19 @@ template <> struct Out4<float> {
     typedef f32x4 T;
     __device__ static T pack(float a, float b, float c, float d) { return T{a, b, c, d}; }
 };
+// A lane's 8 consecutive outputs of one row, written with one store where
+// the granule has no duplicate pixels.
+template <typename TY> struct Out8;
+template <> struct Out8<uint16_t> {
+    typedef u32x4 T;
+    __device__ static T join(u32x2 lo, u32x2 hi) { return T{lo.x, lo.y, hi.x, hi.y}; }
+};
+template <> struct Out8<float> {
+    typedef float T __attribute__((ext_vector_type(8)));
+    __device__ static T join(f32x4 lo, f32x4 hi) {
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+};
 
 // kRP: steps of loads in flight ahead of the multiplied step.  GP: pixels
 // per granule (4: 8-byte loads, a 128-pixel tile; 8: 16-byte loads, a
@@ -227,11 +240,14 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
         if (o >= a.n) continue;
         TY* const yr = yb + int64_t(o) * a.y_c;
         if constexpr (GP == 8) {
+            const typename Out4<TY>::T lo = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+            const typename Out4<TY>::T hi = Out4<TY>::pack(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
             if (dup == 0)
-                *reinterpret_cast<typename Out4<TY>::T*>(yr) = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
-            *reinterpret_cast<typename Out4<TY>::T*>(yr + 4) = Out4<TY>::pack(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
+                store_out(reinterpret_cast<typename Out8<TY>::T*>(yr), Out8<TY>::join(lo, hi));
+            else
+                store_out(reinterpret_cast<typename Out4<TY>::T*>(yr + 4), hi);
         } else {
-            *reinterpret_cast<typename Out4<TY>::T*>(yr) = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+            store_out(reinterpret_cast<typename Out4<TY>::T*>(yr), Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]));
         }
     }
 }

@@ -191,7 +191,7 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
             const int32_t oc = g * N + M::row(lane, r);
-            if (oc < a.n) y[yo[nb] + int64_t(oc) * a.y_c] = acc[nb][r];
+            if (oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
         }
     }
 }

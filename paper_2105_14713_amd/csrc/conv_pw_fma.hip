@@ -205,12 +205,12 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
             if constexpr (V4) {
                 if (yo[0] >= 0) {
                     const f32x4 v = {acc[o][0], acc[o][1], acc[o][2], acc[o][3]};
-                    *reinterpret_cast<f32x4*>(y + yo[0] + int64_t(oc) * a.y_c) = v;
+                    store_out(reinterpret_cast<f32x4*>(y + yo[0] + int64_t(oc) * a.y_c), v);
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < PPT; ++i)
-                    if (yo[i] >= 0) y[yo[i] + int64_t(oc) * a.y_c] = acc[o][i];
+                    if (yo[i] >= 0) store_out(&y[yo[i] + int64_t(oc) * a.y_c], acc[o][i]);
             }
         }
     }

@@ -348,7 +348,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
                     vec_t v;
 #pragma unroll
                     for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, zeros ? 0.f : acc[e][r]);
-                    *reinterpret_cast<vec_t*>(yb + int64_t(o) * a.y_c) = v;
+                    store_out(reinterpret_cast<vec_t*>(yb + int64_t(o) * a.y_c), v);
                 }
             }
         } else {
@@ -361,7 +361,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 #pragma unroll
                 for (int r = 0; r < M::ACC; ++r) {
                     const int32_t o = g * N + M::row(lane, r);
-                    if (o < a.n) y[yb + int64_t(o) * a.y_c] = zeros ? 0.f : acc[e][r];
+                    if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], zeros ? 0.f : acc[e][r]);
                 }
             }
         }
