@@ -215,6 +215,41 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
         }
     };
 
+    // A chunk whose only kept block is its first slot (the last chunk when
+    // kept % CC == 1, e.g. the third input channel of a 3-channel stem) at
+    // N = 32: the two lane groups take two taps of that slot, tap 2 st + kq,
+    // instead of one tap of two slots, half of them empty; a tap past the
+    // kernel reads the second slot's zero row with a zero weight.  Half the
+    // MFMA steps for such a chunk.
+    auto compute_one = [&](int buf) {
+        constexpr int S1 = (KK + 1) / 2;
+        const float* xb = xs + buf * XBUF;
+        const float* db = ds + buf * DBUF + o * KK;
+        auto read = [&](int st, float& av, float (&bv)[NBW]) {
+            const int t0 = 2 * st, t1 = 2 * st + 1;
+            const int q0 = t0 / K, r0 = t0 % K, q1 = t1 / K, r1 = t1 % K;
+            const bool ok1 = t1 < KK;
+            const int32_t xo = kq == 0 ? q0 * Wp + r0 : (ok1 ? q1 * Wp + r1 : CP);
+            const float w0 = db[t0], w1 = ok1 ? db[ok1 ? t1 : t0] : 0.f;
+            av = kq == 0 ? w0 : w1;
+            const float* xj = xb + xo;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) bv[nb] = xj[pofs[nb]];
+        };
+        constexpr int PD = 2;
+        float av[PD + 1], bv[PD + 1][NBW];
+#pragma unroll
+        for (int st = 0; st < PD && st < S1; ++st) read(st, av[st], bv[st]);
+#pragma unroll
+        for (int st = 0; st < S1; ++st) {
+            const int cur = st % (PD + 1);
+            if (st + PD < S1) read(st + PD, av[(st + PD) % (PD + 1)], bv[(st + PD) % (PD + 1)]);
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) acc[nb] = M::step(av[cur], bv[cur][nb], acc[nb]);
+        }
+    };
+    const bool one_last = N == 32 && CC == 2 && kept % CC == 1;
+
     // Chunk c + 1 is staged while chunk c is multiplied; one barrier per chunk
     // hands the buffers over.
     if (nchunks > 0) {
@@ -232,7 +267,8 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
             stage(c + 1, (c + 1) & 1);
             copy_channels(c + 3);
         }
-        compute(c & 1);
+        if (one_last && c == nchunks - 1) compute_one(c & 1);
+        else compute(c & 1);
         vm_wait<0>();
         __syncthreads();
     }

@@ -383,6 +383,7 @@ def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
     dict(k=1, s=2, pd=0, B=3, H=28, W=28, m=45, N=32),   # strided 1x1 (downsample)
     dict(k=1, s=2, pd=0, B=2, H=15, W=9, m=40, N=16),
     dict(k=7, s=2, pd=3, B=2, H=40, W=40, m=3, N=32),    # stem-like: 3 channels
+    dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=32),    # odd kept count after whole chunks
     dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=16),
 ], ids=lambda c: f"k{c['k']}s{c['s']}p{c['pd']}_B{c['B']}_{c['H']}x{c['W']}_m{c['m']}_N{c['N']}")
 def test_kxk_integer_exact(case, tp, monkeypatch):
