@@ -505,8 +505,13 @@ TileShape tile_shape(const ConvArgs& a) {
     for (int sw : {64, 32, 16}) {
         if (sw < (a.N == 32 ? 32 : 16)) continue;
         if (int64_t(a.m) * sw > kTileBufFloats) continue;
+        // Slices per tile: as many as the buffer holds, but once a tile has 8
+        // units not so many that the layer has fewer tiles than compute units
+        // (each workgroup would copy a whole tile for a fraction of its units).
         int sl = 1;
-        while (int64_t(a.m) * sw * sl * 2 <= kTileBufFloats && int64_t(sl) * sw < a.npix && sl < 64)
+        while (int64_t(a.m) * sw * sl * 2 <= kTileBufFloats && int64_t(sl) * sw < a.npix && sl < 64 &&
+               (int64_t(sl) * a.G < 8 ||
+                (int64_t(a.npix) + int64_t(sw) * sl * 2 - 1) / (int64_t(sw) * sl * 2) >= device_cu_count()))
             sl *= 2;
         if (int64_t(sl) * a.G < 8) continue;
         const int64_t tiles = (int64_t(a.npix) + int64_t(sw) * sl - 1) / (int64_t(sw) * sl);
