@@ -121,7 +121,7 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     if (pointwise_applies(a, xdt, ydt, layout)) {
         const bool forced_pw = env_is("ONEXN_PW_KERNEL", "tile") || env_is("ONEXN_PW_KERNEL", "stream");
         const bool prefer_direct = env_is("ONEXN_PW_KERNEL", "direct") || a.m >= a.n || a.npix <= 8192 ||
-                                   (a.N == 32 && a.npix <= 32768 && a.m <= 128) || (a.N == 32 && a.m <= 32);
+                                   (a.N == 32 && a.npix <= 32768 && a.m <= 128);
         if (!direct || forced_pw || !prefer_direct) return launch_pointwise(a, xdt, ydt, s);
     }
     if (direct) return launch_pw_direct(a, s);
