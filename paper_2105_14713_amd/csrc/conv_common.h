@@ -39,6 +39,7 @@ struct ConvArgs {
     int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder)
     int32_t kx_rows;       // k x k staged kernel: output rows per tile,
     int32_t kx_wp, kx_vrwp, kx_cp;   // staged row width, input rows x row width, channel pitch (floats)
+    int32_t kx_tiles;      // and its tile count (balanced split)
 };
 
 // ---------------------------------------------------------------------------

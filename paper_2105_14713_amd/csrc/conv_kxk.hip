@@ -43,8 +43,9 @@ namespace {
 constexpr int kKxWaves = 4;
 constexpr int kKxThreads = 64 * kKxWaves;
 constexpr int kKxMaxRem = 9;   // staged positions per lane per channel: (virtual rows x Wp) <= 9 * 256
+constexpr int kKxSplitMaxG = 256;   // col-groups of a layer the balanced split takes
 
-template <int N, int K, int NBW, int CC>
+template <int N, int K, int NBW, int CC, bool SPLIT>
 __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
@@ -52,22 +53,26 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
     constexpr int DBUF = CC * N * KK;   // floats of one chunk's weights
     static_assert(CC % KS == 0 && DBUF % 64 == 0, "chunk shape");
     extern __shared__ __attribute__((aligned(16))) float smem[];
+    __shared__ int32_t sC[SPLIT ? kKxSplitMaxG + 1 : 1];   // chunks of the col-groups before g
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
-    const int32_t g = L % a.G, tile = L / a.G;
-    int32_t zb, ze;
-    group_range(a, g, zb, ze);
-    const int32_t kept = ze - zb;
     const int32_t R = a.kx_rows, Wp = a.kx_wp, VRWp = a.kx_vrwp, CP = a.kx_cp;
     const int32_t XBUF = CC * CP;
     float* const xs = smem;              // [2][CC][CP]
     float* const ds = smem + 2 * XBUF;   // [2][CC][N][KK]
     int32_t* const sI = reinterpret_cast<int32_t*>(ds + 2 * DBUF);   // [3][64]
+    const int32_t batch = a.npix / a.HWo;
+
+    // Chunks [ca, cb) of the (tile, col-group g) output block; a part of a
+    // block (split) adds its partial sums to y, which holds zeros before.
+    auto run = [&](const int32_t tile, const int32_t g, const int32_t ca, const int32_t cb, const bool split)
+                   __attribute__((always_inline)) {
+    int32_t zb, ze;
+    group_range(a, g, zb, ze);
+    const int32_t kept = ze - zb;
 
     // Output rows of the tile, in batch-major order: [rr0, rr1).
-    const int32_t batch = a.npix / a.HWo;
     const int32_t rr0 = tile * R;
     const int32_t rr1 = min(rr0 + R, batch * a.Ho);
     const int32_t b0 = rr0 / a.Ho, blast = (rr1 - 1) / a.Ho;
@@ -252,18 +257,18 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
 
     // Chunk c + 1 is staged while chunk c is multiplied; one barrier per chunk
     // hands the buffers over.
-    if (nchunks > 0) {
-        copy_channels(0);
-        copy_channels(1);
+    if (cb > ca) {
+        copy_channels(ca);
+        copy_channels(ca + 1);
         vm_wait<0>();
         __syncthreads();
-        stage(0, 0);
-        copy_channels(2);
+        stage(ca, ca & 1);
+        copy_channels(ca + 2);
     }
     vm_wait<0>();
     __syncthreads();
-    for (int32_t c = 0; c < nchunks; ++c) {
-        if (c + 1 < nchunks) {
+    for (int32_t c = ca; c < cb; ++c) {
+        if (c + 1 < cb) {
             stage(c + 1, (c + 1) & 1);
             copy_channels(c + 3);
         }
@@ -281,7 +286,67 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
             const int32_t oc = g * N + M::row(lane, r);
-            if (oc < a.n) store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            if (oc >= a.n) continue;
+            if (SPLIT && split) unsafeAtomicAdd(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            else store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+        }
+    }
+    };
+
+    if constexpr (!SPLIT) {
+        const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
+        const int32_t g = L % a.G, tile = L / a.G;
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        run(tile, g, 0, (ze - zb + CC - 1) / CC, false);
+    } else {
+        // Balanced split: the (tile, col-group, chunk) sequence, tile-major,
+        // is cut into one contiguous range of equal length per workgroup, so
+        // every compute unit gets the same work however the blocks divide
+        // among them.  sC[g]: chunks of the col-groups before g.
+        if (wave == 0) {
+            int32_t carry = 0;
+            for (int32_t g0 = 0; g0 < a.G; g0 += 64) {
+                const int32_t gg = g0 + lane;
+                int32_t v = 0;
+                if (gg < a.G) {
+                    int32_t zb, ze;
+                    group_range(a, gg, zb, ze);
+                    v = (ze - zb + CC - 1) / CC;
+                }
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const int32_t u = __shfl_up(v, d);
+                    if (lane >= d) v += u;
+                }
+                if (gg < a.G) sC[gg + 1] = carry + v;
+                carry += __shfl(v, 63);
+            }
+            if (lane == 0) sC[0] = 0;
+        }
+        __syncthreads();
+        const int32_t G = a.G;
+        const int32_t tcost = __builtin_amdgcn_readfirstlane(sC[G]);   // chunks of one tile
+        const int32_t L = xcd_remap(int32_t(blockIdx.x), a.total);
+        const int64_t total = int64_t(a.kx_tiles) * tcost;
+        int64_t c = total * L / a.total;
+        const int64_t c1 = total * (L + 1) / a.total;
+        while (c < c1) {
+            const int32_t tile = int32_t(c / tcost);
+            const int32_t r = int32_t(c - int64_t(tile) * tcost);
+            int32_t lo = 1, hi = G;   // first j in [1, G] with sC[j] > r
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (sC[mid] > r) hi = mid;
+                else lo = mid + 1;
+            }
+            const int32_t g = __builtin_amdgcn_readfirstlane(lo - 1);
+            const int32_t base = __builtin_amdgcn_readfirstlane(sC[g]);
+            const int32_t nch = __builtin_amdgcn_readfirstlane(sC[g + 1]) - base;
+            const int32_t ca = r - base;
+            const int32_t cb = int32_t(min<int64_t>(nch, ca + (c1 - c)));
+            run(tile, g, ca, cb, ca > 0 || cb < nch);
+            c += cb - ca;
         }
     }
 }
@@ -337,6 +402,30 @@ KxShape kx_shape(const ConvArgs& a, int tp, int cc) {
 
 int kx_cc(int N, int k) { return k == 7 ? (N == 32 ? 2 : 4) : 4; }
 
+// Zeros n floats at p (the output of a balanced-split launch, whose parts of
+// an output block add into it).
+__global__ void __launch_bounds__(256) kx_zero(float* __restrict__ p, int64_t n) {
+    const int64_t stride = int64_t(gridDim.x) * 256 * 4;
+    for (int64_t i = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4; i < n; i += stride) {
+        if (i + 4 <= n) *reinterpret_cast<float4*>(p + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+        else
+            for (int64_t j = i; j < n; ++j) p[j] = 0.f;
+    }
+}
+
+// Workgroups per compute unit of the balanced split (0: one workgroup per
+// output block).  All blocks of a launch are resident at once, so a launch
+// takes as long as its busiest compute unit: with few blocks per unit (800
+// blocks on 256 units: 4 on some, 3.125 on average) that loses up to a
+// quarter.  Measured on the ResNet-50 3x3 layers at batch 64, the split with
+// four workgroups per unit takes 10-21 % off the 128-pixel-tile launches
+// (fewer than 8 blocks per unit) and slows the 256-pixel ones (more
+// registers: 4 waves per SIMD instead of 7), whose blocks are longer.
+int kx_split_choice(const KxShape& s, int64_t units) {
+    if (const char* env = std::getenv("ONEXN_KXK_SPLIT")) return std::atoi(env);   // testing
+    return s.tp == 128 && units < 8 * int64_t(device_cu_count()) ? 4 : 0;
+}
+
 template <int N, int K, int NBW>
 onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
     constexpr int CC = (K == 7) ? (N == 32 ? 2 : 4) : 4;
@@ -345,13 +434,27 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
     a.kx_vrwp = s.vrwp;
     a.kx_cp = s.cp;
     const int64_t nrows = int64_t(a.npix / a.HWo) * a.Ho;
-    const int64_t total = (nrows + s.rows - 1) / s.rows * a.G;
+    const int64_t tiles = (nrows + s.rows - 1) / s.rows;
+    const int64_t total = tiles * a.G;
     if (total < 1 || total > INT32_MAX / kKxThreads)
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: grid of %lld workgroups is out of range",
                     (long long)total);
     a.total = int32_t(total);
+    a.kx_tiles = int32_t(tiles);
     const size_t lds = size_t(kx_lds_bytes(CC, s.cp, N, K * K));
-    hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
+    // (NCHW output, contiguous and 16-byte aligned for the zero fill.)
+    const bool can_split = a.G <= kKxSplitMaxG && a.y_c == a.HWo && reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
+    const int split = can_split ? kx_split_choice(s, total) : 0;
+    if (split > 0) {
+        const int64_t ny = int64_t(a.npix / a.HWo) * a.y_img;
+        const int64_t zb = std::min<int64_t>((ny + 1023) / 1024, 4 * int64_t(device_cu_count()));
+        hipLaunchKernelGGL(kx_zero, dim3(uint32_t(zb)), dim3(256), 0, stream, static_cast<float*>(a.y), ny);
+        // (Ranges shorter than an eighth of a block only add partial sums.)
+        a.total = int32_t(std::min<int64_t>(8 * total, int64_t(split) * device_cu_count()));
+        hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, true>), dim3(uint32_t(a.total)), dim3(kKxThreads), lds, stream, a);
+    } else {
+        hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, false>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
+    }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess)
         return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(err));

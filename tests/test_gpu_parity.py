@@ -402,6 +402,32 @@ def test_kxk_integer_exact(case, tp, monkeypatch):
         np.testing.assert_array_equal(y, ref)
 
 
+@pytest.mark.parametrize("split", ["0", "1", "4"])
+@pytest.mark.parametrize("case", [
+    dict(k=3, s=1, pd=1, B=2, H=56, W=56, m=20, N=32),
+    dict(k=3, s=1, pd=1, B=5, H=14, W=14, m=37, N=32),
+    dict(k=3, s=2, pd=1, B=3, H=28, W=28, m=19, N=32),
+    dict(k=3, s=1, pd=1, B=9, H=7, W=7, m=70, N=16),
+    dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=32),
+    dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=16),
+], ids=lambda c: f"k{c['k']}s{c['s']}p{c['pd']}_B{c['B']}_{c['H']}x{c['W']}_m{c['m']}_N{c['N']}")
+def test_kxk_balanced_split_integer_exact(case, split, monkeypatch):
+    """The k x k kernel with the (tile, col-group, chunk) sequence cut into
+    equal ranges per workgroup: blocks cut into up to eight parts that add
+    into a zeroed output, col-groups with no kept block, and ranges that end
+    inside the last chunk of a col-group."""
+    monkeypatch.setenv("ONEXN_KXK_SPLIT", split)
+    c = case
+    n = 2 * c["N"] + c["N"] // 2
+    w, x = workloads.gen_integer_layer(seed=c["m"] * 5 + c["k"], cout=n, cin=c["m"], k=c["k"],
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=2, xmax=3)
+    print(f"kxk split {c} split={split}", flush=True)
+    for p in (0.0, 0.5, 0.9, 1.0):
+        y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        np.testing.assert_array_equal(y, ref)
+
+
 def test_kxk_matches_generic_on_random_fp32(monkeypatch):
     """Random-valued fp32 3x3 layer: the staged kernel and the oracle agree to
     1e-5 of max |y| over a contraction of 288 * 9 entries."""
