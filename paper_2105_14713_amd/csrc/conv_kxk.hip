@@ -407,9 +407,9 @@ int kx_cc(int N, int k) { return k == 7 ? (N == 32 ? 2 : 4) : 4; }
 __global__ void __launch_bounds__(256) kx_zero(float* __restrict__ p, int64_t n) {
     const int64_t stride = int64_t(gridDim.x) * 256 * 4;
     for (int64_t i = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4; i < n; i += stride) {
-        if (i + 4 <= n) *reinterpret_cast<float4*>(p + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i + 4 <= n) store_out(reinterpret_cast<f32x4*>(p + i), f32x4{0.f, 0.f, 0.f, 0.f});
         else
-            for (int64_t j = i; j < n; ++j) p[j] = 0.f;
+            for (int64_t j = i; j < n; ++j) store_out(p + j, 0.f);
     }
 }
 
