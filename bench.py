@@ -1,17 +1,25 @@
 """Benchmark of the 1xN-pruned convolution forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c1] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2] [--no-cpu]
 
 A step is one forward pass of the workload's pruned layer(s) (Eq. 8 on the
-GPU) over one batch of synthetic input already resident in HBM.  Mask
-building and packing are the offline part of the method (done once per layer
-before deployment) and run before the timed region.  To keep timed steps from
-hitting the 256 MB Infinity Cache with the previous step's data, the input and
-output buffers rotate over enough copies to exceed 512 MB.
+GPU) over one batch of synthetic input already resident in HBM.  The default
+workload is every convolution of a ResNet-50-shaped network at batch 64 in
+fp32 (N = 32, p = 0.5, the 7x7 stem dense).  Mask building and packing are
+the offline part of the method (done once per layer before deployment) and
+run before the timed region.  To keep timed steps from hitting the 256 MB
+Infinity Cache with the previous step's data, the input and output buffers
+rotate over enough copies to exceed 512 MB.
+
+Before anything is timed, every layer's output is checked against the oracle
+on at least 10^4 sampled outputs (random ones plus one in every tile of
+pixels and col-group); a miss exits with status 3 and prints no result.
 
 Prints one JSON line.  value = actual TFLOP/s (2 * pixels * N * kh * kw * t
 per layer, summed) over the timed steps; the dense-equivalent rate and the
-HBM rate are reported beside it.
+HBM rate are reported beside it.  The roofline fraction is the sum over
+layers of each layer's roofline time, max(F_act / peak, B_alg / 8 TB/s),
+divided by the measured step time; per-layer rows give each layer's share.
 """
 import argparse
 import hashlib
@@ -33,6 +41,11 @@ PEAK_HBM_GBPS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
 METRIC = "1×N sparse conv fwd: actual & dense-equiv TFLOP/s, % of MFMA/HBM roofline"
 ROTATE_BYTES = 512 << 20
+DEFAULT_WORKLOAD = "c2"
+PARITY_SAMPLES = 10000
+PAPER_CPU_CONTEXT = ("the paper's only latency figure: 1xN (N = 4) saves 56.04 ms of MobileNet-V2 "
+                     "inference against weight pruning on an Arm Cortex-A7 (Zeropi board, "
+                     "TVM/Ansor); a network latency difference on another machine, not a target")
 
 WORKLOADS = {
     "c0": workloads.config0,
@@ -78,11 +91,11 @@ def source_hash(files):
 
 
 def measured_traffic(workload):
-    """HBM bytes per launch of the workload's kernel from the committed
-    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE in KiB per dispatch,
-    each scaled by the factor the same counter shows for a copy kernel of
-    known size), or None when there is none, or when any source file the
-    kernel is built from (listed in the record) has changed since."""
+    """HBM bytes per step of the workload from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE in KiB, summed over the step's
+    dispatches, each scaled by the factor the same counter shows for a copy
+    kernel of known size), or None when there is none, or when any source
+    file the kernels are built from (listed in the record) has changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
@@ -111,24 +124,68 @@ def copy_calibration(dev):
                       "bytes_written": COPY_BYTES, "launches": 5}), flush=True)
 
 
-def cpu_baseline(layers, batch, wl, budget_s):
-    """The oracle (direct 7-loop over the masked dense weight, fp64) on the host
-    cores, over a bounded sample: single images through all the workload's
-    layers, cycling over the batch until the time budget is spent."""
+def parity_gate(prepared, wl):
+    """Each layer's output (from one launch of the same call the timed steps
+    make) against the oracle at sampled outputs.  Returns per-layer records;
+    exits with status 3 on the first layer over the bar."""
+    import oracle
+    bar = 2e-2 if wl.out_dtype == "bf16" else 1e-5
+    recs = []
+    for li, (layer, packed, xs, ys, w_cpu, x_cpu, call0) in enumerate(prepared):
+        call0()
+        torch.cuda.synchronize()
+        y = ys[0]
+        idx = workloads.sample_outputs(tuple(y.shape), layer.N, PARITY_SAMPLES, seed=li)
+        got = y.reshape(-1)[torch.from_numpy(idx).to(y.device)].double().cpu().numpy()
+        pr = oracle.prune(w_cpu.double().numpy(), layer.N, layer.p, layer.rearrange)
+        ref = oracle.conv2d_at(x_cpu.double().numpy(), pr.wbar, idx, (layer.stride,) * 2,
+                               (layer.pad,) * 2)
+        den = float(abs(ref).max()) if ref.size else 0.0
+        num = float(abs(got - ref).max()) if ref.size else 0.0
+        err = num / den if den > 0 else (0.0 if num == 0 else float("inf"))
+        ok = packed.t == pr.t and err <= bar and bool(torch.isfinite(torch.from_numpy(got)).all())
+        recs.append({"layer": layer.name, "samples": int(idx.size), "rel_err": err, "ok": ok})
+        if not ok:
+            print(json.dumps({"parity": "FAIL", "workload": wl.name, "layer": layer.name,
+                              "t": packed.t, "t_oracle": pr.t, "rel_err": err, "bar": bar,
+                              "samples": int(idx.size)}), flush=True)
+            sys.exit(3)
+    return recs
+
+
+def cpu_rate(lw, budget_s):
+    """Oracle flops (the 1xN kernel's actual flops) per second over single-image
+    passes through all layers until ``budget_s`` seconds are spent."""
     import oracle
     done_f, spent, imgs = 0.0, 0.0, 0
-    lw = []
-    for layer in layers:
-        w, x = workloads.gen_layer(layer, 1, wl.dtype)
-        pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
-        lw.append((layer, pr, x.double().numpy()))
     while spent < budget_s:
         for layer, pr, x in lw:
             t0 = time.perf_counter()
             oracle.conv2d(x, pr.wbar, (layer.stride,) * 2, (layer.pad,) * 2)
             spent += time.perf_counter() - t0
             done_f += 2.0 * layer.Ho * layer.Ho * layer.N * layer.k * layer.k * pr.t
+            if spent >= budget_s:
+                break
         imgs += 1
+    return done_f / spent / 1e12, spent, imgs
+
+
+def cpu_baseline(layers, batch, wl, budget_s, single_budget_s):
+    """The oracle (direct 7-loop over the masked dense weight, fp64) on the host
+    cores, over a bounded sample: single images through the workload's layers,
+    cycling over the layers until the time budget is spent; first on all the
+    threads OpenMP takes, then on one thread."""
+    import oracle
+    lw = []
+    for layer in layers:
+        w, x = workloads.gen_layer(layer, 1, wl.dtype)
+        pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+        lw.append((layer, pr, x.double().numpy()))
+    threads = oracle.num_threads()
+    rate, spent, imgs = cpu_rate(lw, budget_s)
+    oracle.set_num_threads(1)
+    rate1, spent1, imgs1 = cpu_rate(lw, single_budget_s)
+    oracle.set_num_threads(threads)
     cpu_model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -138,12 +195,16 @@ def cpu_baseline(layers, batch, wl, budget_s):
                     break
     except OSError:
         pass
-    return {"value": done_f / spent / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+    return {"value": rate, "unit": "TFLOP/s", "cores": threads,
             "cpu_model": cpu_model, "host_cpus": os.cpu_count(),
             "kind": "oracle",
-            "sample": f"{imgs} single-image passes (the workload has batch {batch}) through all "
-                      f"{len(layers)} layer(s): fp64 direct convolution over the masked dense "
-                      f"weight, {spent:.1f} s; rate counts the 1xN kernel's actual flops"}
+            "sample": f"{imgs} single-image passes (the workload has batch {batch}) over the "
+                      f"workload's {len(layers)} layer(s) in order: fp64 direct convolution over "
+                      f"the masked dense weight, {spent:.1f} s; rate counts the 1xN kernel's "
+                      f"actual flops",
+            "single_thread": {"value": rate1, "unit": "TFLOP/s", "cores": 1,
+                              "sample": f"{imgs1} single-image passes, {spent1:.1f} s"},
+            "paper_context": PAPER_CPU_CONTEXT}
 
 
 def main():
@@ -151,9 +212,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c1", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
+    ap.add_argument("--cpu-single-budget", type=float, default=8.0,
+                    help="seconds of single-threaded oracle work")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a copy kernel of known size (for scaling byte counters)")
     args = ap.parse_args()
@@ -173,11 +236,15 @@ def main():
     wl = WORKLOADS[args.workload]()
     batch = wl.batch
     odt = _TDT[wl.out_dtype]
+    stream = torch.cuda.current_stream(dev)
+    print(f"bench: {wl.name}: preparing {len(wl.layers)} layer(s)", file=sys.stderr, flush=True)
 
     # Offline: generate, build masks, pack, copy to the device.
     prepared = []
+    rows = []
     f_act = f_dense = b_alg = 0.0
     t_host = 0.0
+    peak = PEAK_TFLOPS[wl.dtype]
     for layer in wl.layers:
         w, x = workloads.gen_layer(layer, batch, wl.dtype)
         t0 = time.perf_counter()
@@ -185,22 +252,27 @@ def main():
         t_host += time.perf_counter() - t0
         fa, fd, bb = layer_work(layer, packed, batch, wl.dtype, wl.out_dtype)
         f_act, f_dense, b_alg = f_act + fa, f_dense + fd, b_alg + bb
+        t_c, t_m = fa / (peak * 1e12), bb / (PEAK_HBM_GBPS * 1e9)
+        rows.append({"layer": layer.name, "k": layer.k, "stride": layer.stride, "cin": layer.cin,
+                     "cout": layer.cout, "H": layer.H, "N": layer.N, "p": layer.p, "t": packed.t,
+                     "gflop_act": fa / 1e9, "mb_alg": bb / 1e6,
+                     "bound": "mfma" if t_c >= t_m else "hbm", "t_roof_us": max(t_c, t_m) * 1e6})
         xd = x.to(dev)
         Ho = layer.Ho
         copies = max(1, math.ceil(ROTATE_BYTES / max(bb, 1)))
         copies = min(copies, 16)
         xs = [xd] + [xd.clone() for _ in range(copies - 1)]
         ys = [torch.empty((batch, layer.cout, Ho, Ho), dtype=odt, device=dev) for _ in range(copies)]
-        prepared.append((layer, packed, xs, ys))
-        del x, w
+        calls = [onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
+                                 layer.stride, layer.pad, "nchw", stream.cuda_stream)
+                 for r in range(copies)]
+        prepared.append((layer, packed, xs, ys, w, x, calls))
 
-    stream = torch.cuda.current_stream(dev)
-    # One pre-marshalled launch per (layer, buffer copy); a step issues one per layer.
-    calls = []
-    for layer, packed, xs, ys in prepared:
-        calls.append([onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
-                                      layer.stride, layer.pad, "nchw", stream.cuda_stream)
-                      for r in range(len(xs))])
+    # Parity before timing: the same bound calls the timed steps issue.
+    print("bench: parity gate against the oracle", file=sys.stderr, flush=True)
+    gate = parity_gate([(l, pk, xs, ys, w, x, calls[0]) for l, pk, xs, ys, w, x, calls in prepared], wl)
+    calls = [item[6] for item in prepared]
+    del prepared    # the host copies of the inputs are no longer needed
 
     def step(i):
         for per_layer in calls:
@@ -224,19 +296,23 @@ def main():
     cyc1.record(stream)
     torch.cuda.synchronize()
     cycles_per_ms = 1_000_000 / max(cyc0.elapsed_time(cyc1), 1e-3)
-    stall_ms = 2.0 * host_step_s * 1e3 * (args.steps + 2) + 5.0
 
-    # Timed region: the stream is held by a spin kernel while all K steps (and
-    # an event pair around each) are enqueued, so the GPU then runs them back
-    # to back and the events time the kernels, not the host.
+    def stalled(n_events):
+        """Holds the stream with a spin kernel long enough for the host to
+        enqueue everything that follows, so the GPU runs it back to back."""
+        stall_ms = 2.0 * host_step_s * 1e3 * (args.steps + 2) * n_events + 5.0
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(stall_ms * cycles_per_ms))
+        end = torch.cuda.Event()
+        end.record(stream)
+        return end
+
+    # Timed region: one event pair around each of the K back-to-back steps.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     t_all0 = torch.cuda.Event(enable_timing=True)
     t_all1 = torch.cuda.Event(enable_timing=True)
-    stall_end = torch.cuda.Event()
-    torch.cuda.synchronize()
-    torch.cuda._sleep(int(stall_ms * cycles_per_ms))
-    stall_end.record(stream)
+    stall_end = stalled(1)
     t_all0.record(stream)
     for i in range(args.steps):
         ev[i][0].record(stream)
@@ -250,17 +326,44 @@ def main():
     avg_step_ms = sum(per_step) / len(per_step)
     ms_per_step = total_ms / args.steps
 
-    dtype = wl.dtype
-    peak = PEAK_TFLOPS[dtype]
-    t_compute = f_act / (peak * 1e12)
-    t_hbm = b_alg / (PEAK_HBM_GBPS * 1e9)
-    bound = "mfma" if t_compute >= t_hbm else "hbm"
-    avg_s = avg_step_ms / 1e3
-    if bound == "mfma":
-        achieved, pk, unit = f_act / avg_s / 1e12, peak, "TFLOP/s"
+    # Per-layer times: the same steps again with an event between consecutive
+    # launches (one chain per step, so the layer times add up to the step).
+    per_layer_ms = [0.0] * len(calls)
+    if len(calls) > 1:
+        lsteps = max(5, min(args.steps, 20))
+        chains = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+                  for _ in range(lsteps)]
+        stalled(2)
+        for i in range(lsteps):
+            chains[i][0].record(stream)
+            for li, per_layer in enumerate(calls):
+                per_layer[(args.warmup + i) % len(per_layer)]()
+                chains[i][li + 1].record(stream)
+        torch.cuda.synchronize()
+        for ch in chains:
+            for li in range(len(calls)):
+                per_layer_ms[li] += ch[li].elapsed_time(ch[li + 1]) / lsteps
     else:
-        achieved, pk, unit = b_alg / avg_s / 1e9, PEAK_HBM_GBPS, "GB/s"
-    traffic = measured_traffic(args.workload) if len(wl.layers) == 1 else None
+        per_layer_ms[0] = avg_step_ms
+    for r, t_ms, g in zip(rows, per_layer_ms, gate):
+        r["t_meas_us"] = round(t_ms * 1e3, 2)
+        r["frac"] = round(r["t_roof_us"] / max(t_ms * 1e3, 1e-9), 4)
+        r["t_roof_us"] = round(r["t_roof_us"], 2)
+        r["gflop_act"] = round(r["gflop_act"], 4)
+        r["mb_alg"] = round(r["mb_alg"], 3)
+        r["parity_samples"] = g["samples"]
+        r["parity_rel_err"] = float(f"{g['rel_err']:.3g}")
+
+    dtype = wl.dtype
+    t_roof_sum_us = sum(r["t_roof_us"] for r in rows)
+    t_roof_mfma = sum(r["t_roof_us"] for r in rows if r["bound"] == "mfma")
+    bound = "mfma" if t_roof_mfma >= t_roof_sum_us - t_roof_mfma else "hbm"
+    frac = t_roof_sum_us / (avg_step_ms * 1e3)
+    if bound == "mfma":
+        pk, unit = peak, "TFLOP/s"
+    else:
+        pk, unit = PEAK_HBM_GBPS, "GB/s"
+    traffic = measured_traffic(args.workload)
 
     rec = {
         "metric": METRIC,
@@ -285,16 +388,24 @@ def main():
         "flops_actual_per_step": f_act,
         "flops_dense_per_step": f_dense,
         "bytes_alg_per_step": b_alg,
-        "t_roof_us": round(max(t_compute, t_hbm) * 1e6, 2),
-        "frac_of_roofline": round(max(t_compute, t_hbm) / avg_s, 4),
-        "roofline": {"bound": bound, "achieved": round(achieved, 3), "peak": pk, "unit": unit,
-                     "frac": round(achieved / pk, 4), "traffic": traffic},
+        "t_roof_us": round(t_roof_sum_us, 2),
+        "frac_of_roofline": round(frac, 4),
+        "roofline": {"bound": bound, "achieved": round(frac * pk, 3), "peak": pk, "unit": unit,
+                     "frac": round(frac, 4), "traffic": traffic,
+                     "definition": "sum over layers of max(F_act/peak, B_alg/8 TB/s) over the "
+                                   "measured step time; achieved = frac x peak"},
+        "parity": {"ok": True, "samples_min": min(g["samples"] for g in gate),
+                   "rel_err_max": max(g["rel_err"] for g in gate),
+                   "bar": 2e-2 if wl.out_dtype == "bf16" else 1e-5},
+        "per_layer": rows,
         "host_prepare_s": round(t_host, 3),
         "host_enqueued_ahead": host_ahead,
         "host_launch_us_per_step": round(host_step_s * 1e6, 1),
     }
     if not args.no_cpu:
-        rec["cpu_baseline"] = cpu_baseline(wl.layers, batch, wl, args.cpu_budget)
+        print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(wl.layers, batch, wl, args.cpu_budget,
+                                           args.cpu_single_budget)
     print(json.dumps(rec), flush=True)
 
 

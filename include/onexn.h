@@ -120,7 +120,9 @@ onexn_status onexn_pack(const void* w, onexn_dtype wdt, int32_t n, int32_t m, in
  *         0 <= pad < 16; m*H*W and n*Ho*Wo below 2^31 (per image).
  * Errors: NULL, DTYPE, ARG, SHAPE (Ho or Wo < 1), UNSUPPORTED, HIP (launch
  *         failed).  batch == 0 is a no-op after the checks; x and y may then
- *         be NULL.
+ *         be NULL.  Argument errors enqueue nothing.  A layer computed in two
+ *         launches (an output fill, then the convolution) that gets HIP from
+ *         the second may have left y zeroed.
  */
 onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
                               onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw,
@@ -128,6 +130,27 @@ onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const 
                               onexn_layout layout, int32_t batch, int32_t H, int32_t W,
                               int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
                               void* y_dev, onexn_dtype ydt, void* stream);
+
+/*
+ * Kernel-choice and launch-shape overrides (host, process-wide).
+ *
+ * Not part of the method: these let a caller reach a particular kernel variant
+ * (tests of every variant's parity) or compare variants (A/B timing).  The
+ * library never reads the environment; until a name is set, and after it is
+ * set to -1, the dispatch rules decide.  Names and values:
+ *   "kernel"      1: generic gather kernels for every layer
+ *   "pw_kernel"   1x1 fp32 N = 16/32: 1 resident tile, 2 streamed, 3 register operands
+ *   "pwb_kernel"  1x1 bf16 N = 32: 1 the LDS-queue kernel
+ *   "pw_wpg", "pw_ranges", "pw_wgs", "pwb_wgs", "pwb_gp", "pwb_rp", "direct_kdb",
+ *   "direct_tile", "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp":
+ *                 tile shapes, workgroup counts and pipeline depths of the
+ *                 kernel families (a value the family cannot use falls back to
+ *                 its default, or makes the conv call fail with UNSUPPORTED).
+ * The setting applies to conv calls that start after it returns; changing it
+ * while another thread is inside onexn_conv2d_fwd gives that call either value.
+ * Errors: NULL, ARG (unknown name, value < -1).
+ */
+onexn_status onexn_set_tuning(const char* name, int32_t value);
 
 /* Static name of a status code ("ONEXN_OK", ...); "ONEXN_UNKNOWN" otherwise. */
 const char* onexn_status_string(onexn_status s);

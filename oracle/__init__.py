@@ -20,7 +20,9 @@ Every function takes and returns numpy arrays; weights and activations are
 float64 (fp32 and bf16 values widen exactly).
 """
 from .oracle import (apply_perm, block_scores, conv2d, conv2d_at, decode, filter_norms, filter_perm,
-                     kept_count, masked_weight, num_threads, pack, prune, select)
+                     kept_count, masked_weight, num_threads, pack, prune, select,
+                     set_num_threads)
 
 __all__ = ["apply_perm", "block_scores", "conv2d", "conv2d_at", "decode", "filter_norms", "filter_perm",
-           "kept_count", "masked_weight", "num_threads", "pack", "prune", "select"]
+           "kept_count", "masked_weight", "num_threads", "pack", "prune", "select",
+           "set_num_threads"]

@@ -48,6 +48,16 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Threads the parallel loops below use from now on (timing runs only). */
+void oracle_set_num_threads(int k)
+{
+#ifdef _OPENMP
+    if (k > 0) omp_set_num_threads(k);
+#else
+    (void)k;
+#endif
+}
+
 /* ---------------------------------------------------------------------- */
 /* Sec. 3.3, filter rearrangement (Fig. 2(a)).                             */
 /* ---------------------------------------------------------------------- */

@@ -29,6 +29,7 @@ def _load():
         _build.build()
     lib = ctypes.CDLL(_build.LIB)
     lib.oracle_num_threads.restype = _int
+    lib.oracle_set_num_threads.argtypes = [_int]
     lib.oracle_filter_norms.argtypes = [_f64p, _int, _int, _int, _int, _f64p]
     lib.oracle_filter_perm.argtypes = [_f64p, _int, _int, _int, _int, _int, _i32p]
     lib.oracle_apply_perm.argtypes = [_f64p, _int, _int, _int, _int, _i32p, _f64p]
@@ -53,6 +54,11 @@ def _f64(a):
 
 def num_threads() -> int:
     return _load().oracle_num_threads()
+
+
+def set_num_threads(k: int) -> None:
+    """Threads of the oracle's parallel loops from now on (for timing it)."""
+    _load().oracle_set_num_threads(int(k))
 
 
 def filter_norms(w):

@@ -26,8 +26,8 @@ _STATUS_NAMES = ["ONEXN_OK", "ONEXN_ERR_NULL", "ONEXN_ERR_ARG", "ONEXN_ERR_SHAPE
 F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 
-EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_status_string",
-            "onexn_last_error")
+EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_set_tuning",
+            "onexn_status_string", "onexn_last_error")
 
 _lib = None
 
@@ -59,6 +59,8 @@ def load_library():
                                      [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
                                      [c_vp, ctypes.c_int, c_vp])
     lib.onexn_conv2d_fwd.restype = ctypes.c_int
+    lib.onexn_set_tuning.argtypes = [ctypes.c_char_p, c_i32]
+    lib.onexn_set_tuning.restype = ctypes.c_int
     lib.onexn_status_string.argtypes = [ctypes.c_int]
     lib.onexn_status_string.restype = ctypes.c_char_p
     lib.onexn_last_error.argtypes = []
@@ -73,6 +75,12 @@ def status_string(status: int) -> str:
 
 def last_error() -> str:
     return load_library().onexn_last_error().decode()
+
+
+def set_tuning(name: str, value: int) -> None:
+    """``onexn_set_tuning``: force a kernel variant or launch shape (-1 restores
+    the automatic choice).  For tests and A/B timing."""
+    _check(load_library().onexn_set_tuning(name.encode(), int(value)), "onexn_set_tuning")
 
 
 def _check(status: int, where: str):
@@ -236,4 +244,4 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
 
 __all__ = ["BF16", "BoundConv", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
-           "prepare_layer", "status_string"]
+           "prepare_layer", "set_tuning", "status_string"]

@@ -32,7 +32,6 @@
 // channel l/16 of the quad.  So a lane's A and B addresses differ from step to
 // step by wave-uniform amounts only.  Entries past the col-group's end and
 // channels outside [0, m) stage zero weights and zero inputs.
-#include <cstdlib>
 
 #include "lds_copy.h"
 #include "pw_common.h"
@@ -422,7 +421,7 @@ __global__ void __launch_bounds__(256) kx_zero(float* __restrict__ p, int64_t n)
 // (fewer than 8 blocks per unit) and slows the 256-pixel ones (more
 // registers: 4 waves per SIMD instead of 7), whose blocks are longer.
 int kx_split_choice(const KxShape& s, int64_t units) {
-    if (const char* env = std::getenv("ONEXN_KXK_SPLIT")) return std::atoi(env);   // testing
+    if (tuning(kTuneKxkSplit) >= 0) return tuning(kTuneKxkSplit);
     return s.tp == 128 && units < 8 * int64_t(device_cu_count()) ? 4 : 0;
 }
 
@@ -449,6 +448,9 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
         const int64_t ny = int64_t(a.npix / a.HWo) * a.y_img;
         const int64_t zb = std::min<int64_t>((ny + 1023) / 1024, 4 * int64_t(device_cu_count()));
         hipLaunchKernelGGL(kx_zero, dim3(uint32_t(zb)), dim3(256), 0, stream, static_cast<float*>(a.y), ny);
+        const hipError_t zerr = hipGetLastError();
+        if (zerr != hipSuccess)
+            return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(zerr));
         // (Ranges shorter than an eighth of a block only add partial sums.)
         a.total = int32_t(std::min<int64_t>(8 * total, int64_t(split) * device_cu_count()));
         hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, true>), dim3(uint32_t(a.total)), dim3(kKxThreads), lds, stream, a);
@@ -472,11 +474,9 @@ onexn_status launch_k(ConvArgs a, hipStream_t stream) {
     const int64_t nrows = int64_t(a.npix / a.HWo) * a.Ho;
     const int64_t want = 3 * int64_t(device_cu_count());
     bool big_ok = big.rows > 0 && (nrows + big.rows - 1) / big.rows * a.G >= want;
-    if (const char* env = std::getenv("ONEXN_KXK_TP")) {   // tile capacity override (testing)
-        const int v = std::atoi(env);
-        if (v == 256 && big.rows > 0) big_ok = true;
-        if (v == 128 && small.rows > 0) big_ok = false;
-    }
+    const int32_t tp = tuning(kTuneKxkTp);
+    if (tp == 256 && big.rows > 0) big_ok = true;
+    if (tp == 128 && small.rows > 0) big_ok = false;
     if (big_ok || (big.rows > 0 && small.rows == 0)) return launch_nbw<N, K, NB_BIG>(a, big, stream);
     return launch_nbw<N, K, NB_SMALL>(a, small, stream);
 }

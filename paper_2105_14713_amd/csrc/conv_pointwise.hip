@@ -35,8 +35,6 @@
 //           4n + e of the wave's slice, so a lane reads 4 consecutive pixels.
 //   N = 32: v_mfma_f32_32x32x2f32, 2 kept blocks per step, NB = 2.
 #include <cstdio>
-#include <cstdlib>
-#include <string>
 
 #include "pw_common.h"
 
@@ -336,10 +334,8 @@ __global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
 // narrower layers so that no wave of a workgroup is idle.  ONEXN_PW_WPG
 // overrides it for A/B measurements.
 int choose_wpg(const ConvArgs& a) {
-    if (const char* env = std::getenv("ONEXN_PW_WPG")) {
-        const int v = std::atoi(env);
-        if (v == 1 || v == 2 || v == 4 || v == 8) return v;
-    }
+    const int32_t v = tuning(kTunePwWpg);
+    if (v == 1 || v == 2 || v == 4 || v == 8) return v;
     if (a.G >= 8) return 1;
     if (a.G >= 4) return 2;
     if (a.G >= 2) return 4;
@@ -350,10 +346,7 @@ int choose_wpg(const ConvArgs& a) {
 // (one fits per CU), each walking its range so that its X stream never
 // drains; ONEXN_PW_RANGES overrides the count for A/B measurements.
 int64_t choose_ranges(int64_t tiles, int64_t gsets) {
-    if (const char* env = std::getenv("ONEXN_PW_RANGES")) {
-        const long v = std::atol(env);
-        if (v >= 1) return std::min<int64_t>(v, tiles);
-    }
+    if (tuning(kTunePwRanges) >= 1) return std::min<int64_t>(tuning(kTunePwRanges), tiles);
     const int64_t per_set = std::max<int64_t>(1, int64_t(device_cu_count()) / gsets);
     return std::min<int64_t>(per_set, tiles);
 }
@@ -397,11 +390,10 @@ bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onex
 // ONEXN_PW_KERNEL=stream or =tile forces one of them (for tests and A/B
 // measurements; =tile on a layer it does not fit is an error).
 onexn_status launch_pointwise(ConvArgs a, onexn_dtype, onexn_dtype, hipStream_t s) {
-    const char* env = std::getenv("ONEXN_PW_KERNEL");
-    const std::string force = env ? env : "";
-    if (force == "tile" && !pw_tile_applies(a))
+    const int32_t force = tuning(kTunePwKernel);
+    if (force == 1 && !pw_tile_applies(a))
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: the resident-tile kernel does not fit this layer");
-    if (force != "stream" && pw_tile_applies(a)) return launch_pw_tile(a, s);
+    if (force != 2 && pw_tile_applies(a)) return launch_pw_tile(a, s);
     return a.N == 16 ? launch_pw_n<16>(a, s) : launch_pw_n<32>(a, s);
 }
 

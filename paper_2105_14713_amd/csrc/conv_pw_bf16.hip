@@ -44,7 +44,6 @@
 // step j+1's A and B fragments and step j+2's channel indices.  Entries past
 // a step's end, and channels outside [0, m), read a zero row for both A and
 // B, so they add exactly nothing.
-#include <cstdlib>
 
 #include "lds_copy.h"
 #include "pw_common.h"
@@ -408,10 +407,7 @@ onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     const int64_t ntiles = (batch * gpi + kQGran - 1) / kQGran;
     const int64_t nitems = ntiles * ((a.G + kQWaves - 1) / kQWaves);
     int64_t wgs = nitems;
-    if (const char* env = std::getenv("ONEXN_PWB_WGS")) {   // workgroup count override (testing)
-        const long v = std::atol(env);
-        if (v >= 1) wgs = std::min<int64_t>(v, nitems);
-    }
+    if (tuning(kTunePwbWgs) >= 1) wgs = std::min<int64_t>(tuning(kTunePwbWgs), nitems);
     return launch_grid(pw_bf16<TY>, a, wgs, s, kQThreads);
 }
 

@@ -38,7 +38,6 @@
 // Work split.  A workgroup is 8 waves, one col-group each, over one pixel
 // tile; the workgroups of a tile are consecutive, so they run on one XCD and
 // share the tile's input rows in its L2.
-#include <cstdlib>
 #include <type_traits>
 
 #include "lds_copy.h"
@@ -262,8 +261,8 @@ onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     // (their accumulators take twice the registers), two for 4 (deeper
     // pipelines add registers, not bandwidth).
     int gp = a.HWo >= 8 ? 8 : 4, rp = 0;
-    if (const char* env = std::getenv("ONEXN_PWB_GP")) gp = std::atoi(env);   // testing
-    if (const char* env = std::getenv("ONEXN_PWB_RP")) rp = std::atoi(env);   // testing
+    if (tuning(kTunePwbGp) >= 0) gp = tuning(kTunePwbGp);
+    if (tuning(kTunePwbRp) >= 0) rp = tuning(kTunePwbRp);
     if (gp == 8 && a.HWo >= 8) {
         const int64_t grid = (batch * ((a.HWo + 7) / 8) + kRGran - 1) / kRGran * gsets;
         if (rp == 2) return launch_grid(pw_bf16r<TY, 2, 8>, a, grid, s, kRThreads);

@@ -30,7 +30,6 @@
 // so a wave keeps two batches of loads in flight.  Entries past the wave's
 // range and channels outside [0, m) read zeros (out-of-range buffer offsets),
 // so they add nothing.
-#include <cstdlib>
 
 #include "lds_copy.h"
 #include "pw_common.h"
@@ -206,7 +205,7 @@ onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
     // small batches.
     const int64_t per_wave = a.G > 0 ? a.t / a.G / KSPLIT : 0;
     int kdb = per_wave < 8 * 8 * KS ? 2 : 8;
-    if (const char* env = std::getenv("ONEXN_DIRECT_KDB")) kdb = std::atoi(env);   // testing
+    if (tuning(kTuneDirectKdb) >= 0) kdb = tuning(kTuneDirectKdb);
     if (kdb == 2) return launch_grid(pw_direct<N, NB, KSPLIT, 2>, a, grid, s, kDThreads);
     return launch_grid(pw_direct<N, NB, KSPLIT, 8>, a, grid, s, kDThreads);
 }
@@ -223,7 +222,7 @@ onexn_status launch_n(ConvArgs a, hipStream_t s) {
         return ((int64_t(a.npix) + nb * COLS - 1) / (nb * COLS) * a.G * ks + 3) / 4;
     };
     int choice = 0;
-    if (const char* env = std::getenv("ONEXN_DIRECT_TILE")) choice = std::atoi(env);   // testing
+    if (tuning(kTuneDirectTile) >= 0) choice = tuning(kTuneDirectTile);
     if (choice == 0) {
         if (wgs(2, 1) >= want || avg_kept < 64) choice = 1;
         else if (wgs(1, 1) >= want || avg_kept < 128) choice = 2;

@@ -25,7 +25,6 @@
 // offset is the range-checked vector offset of a buffer load and the channel
 // offset its scalar offset, so a load costs no vector arithmetic and pixels
 // past the last image read zeros.  Channels outside [0, m) contribute nothing.
-#include <cstdlib>
 
 #include "lds_copy.h"
 #include "pw_common.h"
@@ -224,11 +223,11 @@ onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
     const int64_t ntiles = (int64_t(a.npix) + 64 * PPT - 1) / (64 * PPT);
     const int64_t gsets = (a.G + GSW - 1) / GSW;
     int64_t tpw = std::max<int64_t>(1, std::min<int64_t>(16, ntiles * gsets / (8 * int64_t(device_cu_count()))));
-    if (const char* env = std::getenv("ONEXN_FMA_TPW")) tpw = std::max(1, std::atoi(env));   // testing
+    if (tuning(kTuneFmaTpw) >= 0) tpw = std::max(1, tuning(kTuneFmaTpw));
     const int64_t tiles = (ntiles + tpw - 1) / tpw;   // tile runs
     if constexpr (PPT == 4) {
         const bool v4 = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
-                        (reinterpret_cast<uintptr_t>(a.y) & 15) == 0 && !std::getenv("ONEXN_FMA_NO_V4");
+                        (reinterpret_cast<uintptr_t>(a.y) & 15) == 0 && tuning(kTuneFmaNoV4) != 1;
         if (v4) return launch_grid(pw_fma<N, PPT, GSW, true>, a, tiles * gsets, s, kFThreads);
     }
     return launch_grid(pw_fma<N, PPT, GSW, false>, a, tiles * gsets, s, kFThreads);
@@ -245,7 +244,7 @@ onexn_status launch_n(ConvArgs a, hipStream_t s) {
     const int64_t gs4 = (a.G + 3) / 4, gs2 = (a.G + 1) / 2;
     auto tiles = [&](int tp) { return (int64_t(a.npix) + tp - 1) / tp; };
     int choice = 0;
-    if (const char* env = std::getenv("ONEXN_FMA_TILE")) choice = std::atoi(env);   // testing
+    if (tuning(kTuneFmaTile) >= 0) choice = tuning(kTuneFmaTile);
     if (choice == 0) {
         // The widest tile also wins with fewer workgroups (down to ~1.5 per
         // compute unit) unless the col-groups are long (measured on the

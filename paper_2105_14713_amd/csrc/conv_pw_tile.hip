@@ -39,7 +39,6 @@
 //   N = 32: v_mfma_f32_32x32x2f32, 2 kept blocks per step.
 //   NB = SW / (MFMA columns) column blocks per unit: MFMA column n of block e
 //   is pixel NB*n + e of the slice, so a lane reads NB consecutive pixels.
-#include <cstdlib>
 
 #include "pw_common.h"
 
@@ -531,10 +530,7 @@ onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
     const int64_t pt = int64_t(SW) * a.slices;
     const int64_t tiles = (int64_t(a.npix) + pt - 1) / pt;
     int64_t wgs = device_cu_count();
-    if (const char* env = std::getenv("ONEXN_PW_WGS")) {
-        const long v = std::atol(env);
-        if (v >= 1) wgs = v;
-    }
+    if (tuning(kTunePwWgs) >= 1) wgs = tuning(kTunePwWgs);
     // (at most 2^15 workgroups keeps cost_r * L within int32 in the kernel)
     wgs = std::max<int64_t>(1, std::min<int64_t>({wgs, tiles * a.slices * a.G, int64_t(1) << 15}));
     const int64_t total = tiles * a.slices * (int64_t(a.t) + a.G);

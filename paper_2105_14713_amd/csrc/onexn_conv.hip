@@ -2,7 +2,6 @@
 // kernel family (pointwise LDS-shared kernels for 1x1 stride-1 NCHW layers
 // where they apply, the generic gather kernels otherwise).
 #include <atomic>
-#include <cstdlib>
 #include <cstring>
 
 #include "conv_common.h"
@@ -22,13 +21,21 @@ int device_cu_count() {
     return v;
 }
 
-// ONEXN_KERNEL=generic sends every layer the specialised kernels would take
-// to the generic gather kernels instead (for comparing the two).
-bool env_is(const char* name, const char* value) {
-    const char* env = std::getenv(name);
-    return env && std::strcmp(env, value) == 0;
-}
-bool generic_forced() { return env_is("ONEXN_KERNEL", "generic"); }
+namespace {
+
+// Stored as value + 1, so that the zero-initialised array reads kTuneAuto.
+std::atomic<int32_t> g_tuning[kTuneCount];
+const char* const kTuneNames[kTuneCount] = {
+    "kernel", "pw_kernel", "pwb_kernel", "pw_wpg", "pw_ranges", "pw_wgs", "pwb_wgs", "pwb_gp",
+    "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split",
+    "kxk_tp"};
+
+}  // namespace
+
+int32_t tuning(Tune k) { return g_tuning[k].load(std::memory_order_relaxed) - 1; }
+
+// The generic gather kernels for every layer the specialised ones would take.
+bool generic_forced() { return tuning(kTuneKernel) == 1; }
 
 }  // namespace onexn
 
@@ -111,16 +118,17 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
         a.y_pix = n;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (pw_bf16r_applies(a, xdt, ydt, layout) && !env_is("ONEXN_PWB_KERNEL", "queue")) return launch_pw_bf16r(a, ydt, s);
+    if (pw_bf16r_applies(a, xdt, ydt, layout) && tuning(kTunePwbKernel) != 1) return launch_pw_bf16r(a, ydt, s);
     if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
     // fp32 1x1 layers: the LDS-tile pointwise kernels for layers that widen
     // the channels over many pixels, the register-operand kernel for the
     // rest (contractions at least as long as the output is wide, few pixels,
-    // any stride or padding).  ONEXN_PW_KERNEL=tile|stream|direct overrides.
+    // any stride or padding).  The pw_kernel tuning overrides the choice.
     const bool direct = pw_direct_applies(a, xdt, ydt, layout) && !generic_forced();
     if (pointwise_applies(a, xdt, ydt, layout)) {
-        const bool forced_pw = env_is("ONEXN_PW_KERNEL", "tile") || env_is("ONEXN_PW_KERNEL", "stream");
-        const bool prefer_direct = env_is("ONEXN_PW_KERNEL", "direct") || a.m >= a.n || a.npix <= 8192 ||
+        const int32_t pwk = tuning(kTunePwKernel);
+        const bool forced_pw = pwk == 1 || pwk == 2;
+        const bool prefer_direct = pwk == 3 || a.m >= a.n || a.npix <= 8192 ||
                                    (a.N == 32 && a.npix <= 32768 && a.m <= 128);
         if (!direct || forced_pw || !prefer_direct) return launch_pointwise(a, xdt, ydt, s);
     }
@@ -128,4 +136,17 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     return launch_generic(a, xdt, ydt, s);
+}
+
+extern "C" onexn_status onexn_set_tuning(const char* name, int32_t value) {
+    clear_error();
+    if (!name) return fail(ONEXN_ERR_NULL, "set_tuning: NULL name");
+    if (value < kTuneAuto || value == INT32_MAX)
+        return fail(ONEXN_ERR_ARG, "set_tuning: value %d out of range", value);
+    for (int k = 0; k < kTuneCount; ++k)
+        if (std::strcmp(name, kTuneNames[k]) == 0) {
+            g_tuning[k].store(value + 1, std::memory_order_relaxed);
+            return ONEXN_OK;
+        }
+    return fail(ONEXN_ERR_ARG, "set_tuning: unknown name \"%s\"", name);
 }

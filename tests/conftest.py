@@ -19,3 +19,19 @@ def oracle_lib():
     if not os.path.exists(build.LIB):
         build.build()
     return oracle
+
+
+@pytest.fixture
+def tune():
+    """Sets kernel-choice overrides of the library for one test
+    (``onexn_set_tuning``) and restores the automatic choice afterwards."""
+    import paper_2105_14713_amd as onexn
+    names = []
+
+    def set_(name, value):
+        onexn.set_tuning(name, int(value))
+        names.append(name)
+
+    yield set_
+    for name in names:
+        onexn.set_tuning(name, -1)

@@ -5,6 +5,7 @@ import torch
 
 import oracle
 import paper_2105_14713_amd as onexn
+import workloads
 
 
 def rel_err(y, ref):
@@ -44,14 +45,7 @@ def oracle_conv(w, x_nchw, N, p, rearrange, stride, pad):
 
 
 def sample_indices(shape, count, seed, N):
-    """Random flat NCHW output indices plus the corners and the last (possibly
-    ragged) col-group's rows."""
-    B, n, Ho, Wo = shape
-    total = B * n * Ho * Wo
-    rng = np.random.default_rng(seed)
-    idx = rng.integers(0, total, size=count)
-    extra = [0, total - 1, (n - 1) * Ho * Wo, ((B - 1) * n + (n - 1)) * Ho * Wo + Ho * Wo - 1]
-    g_last = (n - 1) // N * N
-    for o in range(g_last, n):
-        extra.append(((B - 1) * n + o) * Ho * Wo + (Ho * Wo) // 2)
-    return np.unique(np.concatenate([idx, np.array(extra, np.int64)]))
+    """Flat NCHW output indices for a sampled check: ``count`` random ones, one in
+    every (pixel tile, col-group) cell, the corners and the last col-group's rows
+    (``workloads.sample_outputs``)."""
+    return workloads.sample_outputs(shape, N, count, seed)

@@ -205,7 +205,7 @@ def test_runs_on_a_side_stream():
 # configuration as the benchmark), checked on sampled outputs.
 # ---------------------------------------------------------------------------
 
-def _check_sampled(layer, batch, dtype, out_dtype, y, pr, x_cpu, count=3000, seed=0):
+def _check_sampled(layer, batch, dtype, out_dtype, y, pr, x_cpu, count=10000, seed=0):
     idx = sample_indices(tuple(y.shape), count, seed, layer.N)
     got = y.float().reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
     ref = oracle.conv2d_at(x_cpu.double().numpy(), pr.wbar, idx, (layer.stride,) * 2,
@@ -245,7 +245,7 @@ def test_config1_full_size_sampled():
 def test_config4_full_size_sampled(out_dtype):
     wl = workloads.config4(out_dtype)
     y, pr, x = _run_layer(wl.layers[0], wl.batch, "bf16", out_dtype)
-    _check_sampled(wl.layers[0], wl.batch, "bf16", out_dtype, y, pr, x, count=4000)
+    _check_sampled(wl.layers[0], wl.batch, "bf16", out_dtype, y, pr, x)
 
 
 _R50 = workloads.resnet50_convs()
@@ -256,7 +256,7 @@ def test_config2_resnet50_layer_sampled(li):
     layer = _R50[li]
     print(f"resnet50 layer {layer.name}", flush=True)
     y, pr, x = _run_layer(layer, 64)
-    _check_sampled(layer, 64, "f32", "f32", y, pr, x, count=1500, seed=li)
+    _check_sampled(layer, 64, "f32", "f32", y, pr, x, seed=li)
 
 
 _MB = workloads.mobilenet_v2_pointwise(4, 0.5)
@@ -278,7 +278,7 @@ def test_config3_mobilenet_v2_layer_sampled(li):
             torch.cuda.synchronize()
             pr = oracle.prune(w.double().numpy(), N, p, False)
             assert packed.t == pr.t
-            idx = sample_indices(tuple(y.shape), 600, li * 31 + N, N)
+            idx = sample_indices(tuple(y.shape), 10000, li * 31 + N, N)
             got = y.reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
             ref = oracle.conv2d_at(x64, pr.wbar, idx)
             assert rel_err(got, ref) <= 1e-5, (base.name, N, p)
@@ -287,14 +287,14 @@ def test_config3_mobilenet_v2_layer_sampled(li):
 @pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
 @pytest.mark.parametrize("wpg", ["1", "2", "4", "8"])
 @pytest.mark.parametrize("N", [16, 32])
-def test_pointwise_variants_integer_exact(N, wpg, hw, monkeypatch):
+def test_pointwise_variants_integer_exact(N, wpg, hw, tune):
     """Every waves-per-col-group variant of the streamed pointwise kernel:
     several channel chunks with a ragged last one (m = 300 > the largest
     chunk), col-group sets with a partial last set and a ragged last
     col-group, and p from dense to nearly empty (col-groups with no entries in
     some chunks)."""
-    monkeypatch.setenv("ONEXN_PW_KERNEL", "stream")
-    monkeypatch.setenv("ONEXN_PW_WPG", wpg)
+    tune("pw_kernel", 2)
+    tune("pw_wpg", wpg)
     n = 9 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=N, cout=n, cin=300, k=1, batch=2, H=hw[0], W=hw[1],
                                        wmax=1, xmax=2)
@@ -306,28 +306,32 @@ def test_pointwise_variants_integer_exact(N, wpg, hw, monkeypatch):
 
 @pytest.mark.parametrize("wgs", ["1", "5", "default"])
 @pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
-@pytest.mark.parametrize("m", [200, 400, 900], ids=["m200", "m400", "m900"])
-@pytest.mark.parametrize("groups", [10, 2], ids=["G10", "G2"])
-@pytest.mark.parametrize("N", [16, 32])
-def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
-    """The resident-tile pointwise kernel at each slice width (m = 200, 400,
-    900 select 64-, 32- and 16-pixel slices), several slices per tile (two
-    col-groups), a ragged last col-group and ragged pixel tail, pixel rows
-    that do and do not allow 16-byte copies, and workgroup counts that cut the
-    cost ranges inside tiles (1, 5 and the default)."""
-    monkeypatch.setenv("ONEXN_PW_KERNEL", "tile")
+@pytest.mark.parametrize("N,groups,m", [
+    (16, 10, 200),   # 64-pixel slices
+    (16, 10, 400),   # 32-pixel slices
+    (16, 10, 900),   # 16-pixel slices
+    (16, 2, 200),    # 16-pixel slices, 4 slices per tile
+    (32, 10, 200),   # 64-pixel slices
+    (32, 10, 400),   # 32-pixel slices
+    (32, 8, 120),    # 64-pixel slices, exactly 8 units per tile
+    (32, 4, 120),    # 64-pixel slices, 2 slices per tile
+], ids=lambda v: str(v))
+def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, tune):
+    """The resident-tile pointwise kernel at each slice width, with one and
+    several slices per tile, a ragged last col-group and ragged pixel tail,
+    pixel rows that do and do not allow 16-byte copies, and workgroup counts
+    that cut the cost ranges inside tiles (1, 5 and the default).  Every case
+    is a shape the kernel takes (forcing it on one it does not fit is an
+    error, not a skip)."""
+    tune("pw_kernel", 1)
     if wgs != "default":
-        monkeypatch.setenv("ONEXN_PW_WGS", wgs)
+        tune("pw_wgs", wgs)
     n = (groups - 1) * N + N // 2
     w, x = workloads.gen_integer_layer(seed=N + m, cout=n, cin=m, k=1, batch=2, H=hw[0], W=hw[1],
                                        wmax=1, xmax=2)
     print(f"pw tile N={N} n={n} m={m} hw={hw} wgs={wgs}", flush=True)
     for p in (0.0, 0.5, 0.95):
-        try:
-            y, _ = gpu_conv(w, x, N, p, True, 1, 0)
-        except onexn.OnexnError as e:
-            assert e.status == 5   # ONEXN_ERR_UNSUPPORTED: the tile kernel does not fit
-            pytest.skip("resident-tile kernel does not fit this shape")
+        y, _ = gpu_conv(w, x, N, p, True, 1, 0)
         ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
         np.testing.assert_array_equal(y, ref)
 
@@ -340,7 +344,7 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, monkeypatch):
     dict(m=700, B=1, H=8, W=6),      # long contraction: several pipeline periods and a tail
     dict(m=2100, B=1, H=4, W=4),     # more input channels than the register kernel stages
 ], ids=["m300", "m64", "m45", "m700", "m2100"])
-def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
+def test_pw_bf16_integer_exact(shape, variant, tune):
     """The bf16 pointwise kernels (1x1, N = 32, pixels per image a multiple of
     4): the register-gathered kernel with 4-pixel granules at pipeline depths
     2, 4, 6 and with 8-pixel granules at depths 1, 2 (images of 12 and 196
@@ -353,12 +357,12 @@ def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
     cut short where 16 kept channels span more chunks than LDS holds), and
     workgroup counts that give each workgroup several work items."""
     if variant.startswith("g"):
-        monkeypatch.setenv("ONEXN_PWB_GP", variant[1])
-        monkeypatch.setenv("ONEXN_PWB_RP", variant[4:])
+        tune("pwb_gp", variant[1])
+        tune("pwb_rp", variant[4:])
     else:
-        monkeypatch.setenv("ONEXN_PWB_KERNEL", "queue")
+        tune("pwb_kernel", 1)
         if variant != "queue":
-            monkeypatch.setenv("ONEXN_PWB_WGS", variant[5:])
+            tune("pwb_wgs", variant[5:])
     c = shape
     n = 9 * 32 + 16
     w, x = workloads.gen_integer_layer(seed=c["m"] + int(c["B"]), cout=n, cin=c["m"], k=1,
@@ -386,11 +390,11 @@ def test_pw_bf16_integer_exact(shape, variant, monkeypatch):
     dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=32),    # odd kept count after whole chunks
     dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=16),
 ], ids=lambda c: f"k{c['k']}s{c['s']}p{c['pd']}_B{c['B']}_{c['H']}x{c['W']}_m{c['m']}_N{c['N']}")
-def test_kxk_integer_exact(case, tp, monkeypatch):
+def test_kxk_integer_exact(case, tp, tune):
     """The LDS-staged k x k kernel at both tile sizes: tiles of whole output
     rows that span images, padding and stride, ragged last col-group, and p
     from dense to nearly empty (chunks with fewer kept blocks than a step)."""
-    monkeypatch.setenv("ONEXN_KXK_TP", tp)
+    tune("kxk_tp", tp)
     c = case
     n = 2 * c["N"] + c["N"] // 2
     w, x = workloads.gen_integer_layer(seed=c["m"] * 7 + c["k"], cout=n, cin=c["m"], k=c["k"],
@@ -411,12 +415,12 @@ def test_kxk_integer_exact(case, tp, monkeypatch):
     dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=32),
     dict(k=7, s=2, pd=3, B=2, H=33, W=30, m=5, N=16),
 ], ids=lambda c: f"k{c['k']}s{c['s']}p{c['pd']}_B{c['B']}_{c['H']}x{c['W']}_m{c['m']}_N{c['N']}")
-def test_kxk_balanced_split_integer_exact(case, split, monkeypatch):
+def test_kxk_balanced_split_integer_exact(case, split, tune):
     """The k x k kernel with the (tile, col-group, chunk) sequence cut into
     equal ranges per workgroup: blocks cut into up to eight parts that add
     into a zeroed output, col-groups with no kept block, and ranges that end
     inside the last chunk of a col-group."""
-    monkeypatch.setenv("ONEXN_KXK_SPLIT", split)
+    tune("kxk_split", split)
     c = case
     n = 2 * c["N"] + c["N"] // 2
     w, x = workloads.gen_integer_layer(seed=c["m"] * 5 + c["k"], cout=n, cin=c["m"], k=c["k"],
@@ -428,7 +432,7 @@ def test_kxk_balanced_split_integer_exact(case, split, monkeypatch):
         np.testing.assert_array_equal(y, ref)
 
 
-def test_kxk_matches_generic_on_random_fp32(monkeypatch):
+def test_kxk_matches_generic_on_random_fp32():
     """Random-valued fp32 3x3 layer: the staged kernel and the oracle agree to
     1e-5 of max |y| over a contraction of 288 * 9 entries."""
     gen = torch.Generator().manual_seed(11)
@@ -440,7 +444,7 @@ def test_kxk_matches_generic_on_random_fp32(monkeypatch):
 
 
 @pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma", "pwfma", "direct"])
-def test_reads_stay_inside_I_and_D(kind, monkeypatch):
+def test_reads_stay_inside_I_and_D(kind, tune):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
     t would put NaN into the output."""
@@ -449,7 +453,7 @@ def test_reads_stay_inside_I_and_D(kind, monkeypatch):
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
                       "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
     if kind in ("tile", "stream", "direct"):
-        monkeypatch.setenv("ONEXN_PW_KERNEL", kind)
+        tune("pw_kernel", {"tile": 1, "stream": 2, "direct": 3}[kind])
     n = 3 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=7, cout=n, cin=m, k=k, batch=2, H=H, wmax=2, xmax=2)
     w, x = w.to(dt), x.to(dt)
@@ -476,11 +480,11 @@ def test_reads_stay_inside_I_and_D(kind, monkeypatch):
     dict(N=4, m=20, n=50, B=3, H=12, W=10),      # pixels per image a multiple of 4 (16-byte path)
     dict(N=8, m=16, n=72, B=5, H=28, W=28),
 ], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}")
-def test_pw_fma_integer_exact(case, tile, monkeypatch):
+def test_pw_fma_integer_exact(case, tile, tune):
     """The 1x1 FMA kernel at every tile shape (pixels per lane, col-groups per
     workgroup, waves splitting a contraction), with a partial last set of
     col-groups and p from dense to nearly empty."""
-    monkeypatch.setenv("ONEXN_FMA_TILE", tile)
+    tune("fma_tile", tile)
     c = case
     w, x = workloads.gen_integer_layer(seed=c["m"] + c["N"], cout=c["n"], cin=c["m"], k=1,
                                        batch=c["B"], H=c["H"], W=c["W"], wmax=1, xmax=2)
@@ -499,15 +503,15 @@ def test_pw_fma_integer_exact(case, tile, monkeypatch):
     dict(N=32, m=700, n=40, B=2, H=7, W=7, s=1, pd=0),    # long contraction, few pixels
     dict(N=16, m=33, n=20, B=1, H=10, W=13, s=3, pd=2),
 ], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
-def test_pw_direct_integer_exact(case, tile, kdb, monkeypatch):
+def test_pw_direct_integer_exact(case, tile, kdb, tune):
     """The 1x1 kernel with register-loaded operands at every tile shape
     (column blocks per unit, waves splitting the contraction) and both batch
     sizes (2 and 8 MFMA steps; odd batch counts run a batch of zeros):
     strides, padding, ragged col-groups and pixel tails, p from dense to
     nearly empty."""
-    monkeypatch.setenv("ONEXN_DIRECT_TILE", tile)
-    monkeypatch.setenv("ONEXN_DIRECT_KDB", kdb)
-    monkeypatch.setenv("ONEXN_PW_KERNEL", "direct")
+    tune("direct_tile", tile)
+    tune("direct_kdb", kdb)
+    tune("pw_kernel", 3)
     c = case
     w, x = workloads.gen_integer_layer(seed=c["m"] + c["n"], cout=c["n"], cin=c["m"], k=1,
                                        batch=c["B"], H=c["H"], W=c["W"], wmax=1, xmax=2)
