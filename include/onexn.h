@@ -43,6 +43,7 @@ typedef enum {
 
 typedef enum { ONEXN_F32 = 0, ONEXN_BF16 = 1 } onexn_dtype;
 typedef enum { ONEXN_NCHW = 0, ONEXN_NHWC = 1 } onexn_layout;
+typedef enum { ONEXN_ACT_NONE = 0, ONEXN_ACT_RELU = 1, ONEXN_ACT_RELU6 = 2 } onexn_act;
 
 /*
  * Mask building (host, synchronous).
@@ -130,6 +131,33 @@ onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const 
                               onexn_layout layout, int32_t batch, int32_t H, int32_t W,
                               int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
                               void* y_dev, onexn_dtype ydt, void* stream);
+
+/*
+ * The same convolution with a fused epilogue in its store stage (device,
+ * asynchronous): for output channel o (rearranged order) and every pixel,
+ *   y = act(scale[o] * acc + bias[o])
+ * computed in fp32 from the fp32 accumulator, then rounded to ydt.  This is
+ * the per-channel affine map of a batch norm folded for inference (or a plain
+ * bias) followed by ReLU or ReLU6, the layer-to-layer step of the networks
+ * the paper prunes (Sec. 4.1).  Sec. 3.3 requires that every per-channel
+ * parameter of the layer follows the filter rearrangement: scale and bias are
+ * indexed by the rearranged channel, i.e. scale_dev[o] = scale_orig[perm[o]],
+ * and the next layer takes its input channels as W2[:, perm]; the network is
+ * then unchanged.
+ *
+ * scale_dev, bias_dev: device fp32[n], or NULL for 1 and 0.  act: ONEXN_ACT_*.
+ * Every other argument, the result layout and the errors are those of
+ * onexn_conv2d_fwd (plus ARG for an unknown act); with NULL, NULL,
+ * ONEXN_ACT_NONE the result equals onexn_conv2d_fwd's bit for bit.
+ */
+onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                                    onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw,
+                                    int32_t N, int64_t t, const void* x_dev, onexn_dtype xdt,
+                                    onexn_layout layout, int32_t batch, int32_t H, int32_t W,
+                                    int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                    int32_t pad_w, void* y_dev, onexn_dtype ydt,
+                                    const float* scale_dev, const float* bias_dev, onexn_act act,
+                                    void* stream);
 
 /*
  * Kernel-choice and launch-shape overrides (host, process-wide).

@@ -304,6 +304,34 @@ void oracle_conv2d_at(const double* x, const double* wbar, int B, int m, int H, 
 }
 
 /* ---------------------------------------------------------------------- */
+/* The layer-to-layer step after the convolution (Sec. 4.1 networks).      */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * In place on y[B][n][hw]: y = act(scale[o] * y + bias[o]) for output channel
+ * o, i.e. a batch norm folded for inference (or a bias) and then ReLU
+ * (act = 1: max(y, 0)) or ReLU6 (act = 2: min(max(y, 0), 6)); act = 0 leaves
+ * the affine value.  scale == NULL means 1, bias == NULL means 0.  Per Sec.
+ * 3.3 a rearranged layer's channel o is original channel perm[o], so the
+ * caller passes the parameters in the same order as the output channels.
+ */
+void oracle_epilogue(double* y, int B, int n, int64_t hw, const double* scale, const double* bias,
+                     int act)
+{
+    for (int b = 0; b < B; b++)
+        for (int o = 0; o < n; o++)
+            for (int64_t i = 0; i < hw; i++) {
+                double* v = &y[((int64_t)b * n + o) * hw + i];
+                double u = *v;
+                if (scale) u = u * scale[o];
+                if (bias) u = u + bias[o];
+                if (act >= 1 && u < 0.0) u = 0.0;
+                if (act == 2 && u > 6.0) u = 6.0;
+                *v = u;
+            }
+}
+
+/* ---------------------------------------------------------------------- */
 /* Eq. 8: block-wise decode over the BSR arrays.                           */
 /* ---------------------------------------------------------------------- */
 

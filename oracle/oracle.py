@@ -43,6 +43,8 @@ def _load():
     lib.oracle_pack.restype = ctypes.c_int64
     lib.oracle_conv2d.argtypes = [_f64p, _f64p] + [_int] * 11 + [_f64p]
     lib.oracle_conv2d_at.argtypes = [_f64p, _f64p] + [_int] * 11 + [_i64p, ctypes.c_int64, _f64p]
+    lib.oracle_epilogue.argtypes = [_f64p, _int, _int, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_void_p, _int]
     lib.oracle_decode.argtypes = [_f64p, _i32p, _i32p, _f64p] + [_int] * 12 + [_f64p]
     _lib = lib
     return lib
@@ -153,6 +155,24 @@ def conv2d_at(x, wbar, idx, stride=(1, 1), pad=(0, 0)):
     _load().oracle_conv2d_at(x, wbar, B, m, H, W, n, h, wd, stride[0], stride[1], pad[0], pad[1],
                              idx, idx.size, out)
     return out
+
+
+_ACTS = {"none": 0, "relu": 1, "relu6": 2}
+
+
+def epilogue(y, scale=None, bias=None, act="none"):
+    """act(scale[o] * y + bias[o]) per output channel o of y[B][n][Ho][Wo]
+    (a new fp64 array); None means scale 1 / bias 0."""
+    y = np.array(y, dtype=np.float64, order="C", copy=True)
+    B, n = y.shape[0], y.shape[1]
+    hw = int(np.prod(y.shape[2:])) if y.ndim > 2 else 1
+    s = None if scale is None else _f64(scale)
+    b = None if bias is None else _f64(bias)
+    for v in (s, b):
+        assert v is None or v.size == n
+    _load().oracle_epilogue(y, B, n, hw, None if s is None else s.ctypes.data,
+                            None if b is None else b.ctypes.data, _ACTS[act])
+    return y
 
 
 def decode(x, P, I, D, n, stride=(1, 1), pad=(0, 0)):

@@ -26,8 +26,9 @@ _STATUS_NAMES = ["ONEXN_OK", "ONEXN_ERR_NULL", "ONEXN_ERR_ARG", "ONEXN_ERR_SHAPE
 F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 
-EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_set_tuning",
-            "onexn_status_string", "onexn_last_error")
+EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
+            "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
+ACTS = {"none": 0, "relu": 1, "relu6": 2}
 
 _lib = None
 
@@ -59,6 +60,10 @@ def load_library():
                                      [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
                                      [c_vp, ctypes.c_int, c_vp])
     lib.onexn_conv2d_fwd.restype = ctypes.c_int
+    lib.onexn_conv2d_fwd_fused.argtypes = ([c_vp, c_vp, c_vp, ctypes.c_int] + [c_i32] * 5 + [c_i64] +
+                                           [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
+                                           [c_vp, ctypes.c_int, c_vp, c_vp, ctypes.c_int, c_vp])
+    lib.onexn_conv2d_fwd_fused.restype = ctypes.c_int
     lib.onexn_set_tuning.argtypes = [ctypes.c_char_p, c_i32]
     lib.onexn_set_tuning.restype = ctypes.c_int
     lib.onexn_status_string.argtypes = [ctypes.c_int]
@@ -146,11 +151,28 @@ def _pair(v):
     return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
 
 
+def _epilogue_args(n, scale, bias, act):
+    """(scale ptr, bias ptr, act code, fused?) for the fused entry point."""
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}")
+    for name, v in (("scale", scale), ("bias", bias)):
+        if v is not None and (v.device.type != "cuda" or v.dtype != torch.float32 or
+                              not v.is_contiguous() or v.numel() != n):
+            raise ValueError(f"{name} must be a contiguous float32 device tensor of {n} entries")
+    fused = scale is not None or bias is not None or act != "none"
+    return (scale.data_ptr() if scale is not None else 0, bias.data_ptr() if bias is not None else 0,
+            ACTS[act], fused)
+
+
 def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
                stride=1, pad=0, layout: str = "nchw", out_dtype: Optional[torch.dtype] = None,
-               out: Optional[torch.Tensor] = None, stream: Optional[int] = None) -> torch.Tensor:
+               out: Optional[torch.Tensor] = None, stream: Optional[int] = None,
+               scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
+               act: str = "none") -> torch.Tensor:
     """``onexn_conv2d_fwd`` on device tensors; enqueued on ``stream`` (default:
-    torch's current stream), no synchronisation.  Returns y (rearranged channel order)."""
+    torch's current stream), no synchronisation.  Returns y (rearranged channel order).
+    With ``scale``, ``bias`` (fp32 [n], rearranged channel order) or ``act``
+    ("relu", "relu6") it calls ``onexn_conv2d_fwd_fused``: y = act(scale * acc + bias)."""
     for name, tns in (("P", P), ("I", I), ("D", D), ("x", x)):
         if tns.device.type != "cuda":
             raise ValueError(f"{name} must be a device tensor (the convolution only runs on the GPU)")
@@ -176,10 +198,14 @@ def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: tor
         raise ValueError("out has the wrong shape, dtype or layout")
     if stream is None:
         stream = torch.cuda.current_stream(x.device).cuda_stream
+    sp, bp, ac, fused = _epilogue_args(int(n), scale, bias, act)
     args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype),
             int(n), m, kh, kw, N, t, x.data_ptr(), _dtype_code(x.dtype), lay, B, H, W, stride[0],
-            stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt), stream)
-    _check(load_library().onexn_conv2d_fwd(*args), "onexn_conv2d_fwd")
+            stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt))
+    if fused:
+        _check(load_library().onexn_conv2d_fwd_fused(*args, sp, bp, ac, stream), "onexn_conv2d_fwd_fused")
+    else:
+        _check(load_library().onexn_conv2d_fwd(*args, stream), "onexn_conv2d_fwd")
     return out
 
 
@@ -188,20 +214,28 @@ class BoundConv:
     re-issues the same launch (same tensors, same stream).  The tensors must
     stay alive and unmoved while this object is used."""
 
-    def __init__(self, P, I, D, n, x, out, stride=1, pad=0, layout="nchw", stream=None):
-        conv2d_fwd(P, I, D, n, x, stride, pad, layout, out.dtype, out, stream)   # validates
+    def __init__(self, P, I, D, n, x, out, stride=1, pad=0, layout="nchw", stream=None,
+                 scale=None, bias=None, act="none"):
+        conv2d_fwd(P, I, D, n, x, stride, pad, layout, out.dtype, out, stream, scale, bias,
+                   act)   # validates
         t, N, kh, kw = D.shape
         lay = {"nchw": NCHW, "nhwc": NHWC}[layout]
         B, m, H, W = x.shape if lay == NCHW else (x.shape[0], x.shape[3], x.shape[1], x.shape[2])
         stride, pad = _pair(stride), _pair(pad)
         if stream is None:
             stream = torch.cuda.current_stream(x.device).cuda_stream
-        self._keep = (P, I, D, x, out)
-        self._fn = load_library().onexn_conv2d_fwd
+        self._keep = (P, I, D, x, out, scale, bias)
+        sp, bp, ac, fused = _epilogue_args(int(n), scale, bias, act)
         self._args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0,
                       _dtype_code(D.dtype), int(n), m, kh, kw, N, t, x.data_ptr(),
                       _dtype_code(x.dtype), lay, B, H, W, stride[0], stride[1], pad[0], pad[1],
-                      out.data_ptr(), _dtype_code(out.dtype), stream)
+                      out.data_ptr(), _dtype_code(out.dtype))
+        if fused:
+            self._fn = load_library().onexn_conv2d_fwd_fused
+            self._args += (sp, bp, ac, stream)
+        else:
+            self._fn = load_library().onexn_conv2d_fwd
+            self._args += (stream,)
 
     def __call__(self):
         st = self._fn(*self._args)
@@ -224,9 +258,10 @@ class PackedLayer:
     I: torch.Tensor      # device int32[t]
     D: torch.Tensor      # device [t][N][kh][kw]
 
-    def forward(self, x, stride=1, pad=0, layout="nchw", out_dtype=None, out=None, stream=None):
+    def forward(self, x, stride=1, pad=0, layout="nchw", out_dtype=None, out=None, stream=None,
+                scale=None, bias=None, act="none"):
         return conv2d_fwd(self.P, self.I, self.D, self.n, x, stride, pad, layout, out_dtype, out,
-                          stream)
+                          stream, scale, bias, act)
 
 
 def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
@@ -242,6 +277,6 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
     return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
 
 
-__all__ = ["BF16", "BoundConv", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
+__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
            "prepare_layer", "set_tuning", "status_string"]

@@ -40,6 +40,11 @@ struct ConvArgs {
     int32_t kx_rows;       // k x k staged kernel: output rows per tile,
     int32_t kx_wp, kx_vrwp, kx_cp;   // staged row width, input rows x row width, channel pitch (floats)
     int32_t kx_tiles;      // and its tile count (balanced split)
+    // Fused epilogue of the store stage: y = act(scale[o] * acc + bias[o]) for
+    // output channel o (rearranged order); either array may be absent.
+    const float* ep_scale;
+    const float* ep_bias;
+    int32_t ep_act;        // onexn_act
 };
 
 // ---------------------------------------------------------------------------
@@ -69,6 +74,34 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { return f32_to_bf16(v); }
+
+// The fused epilogue on one accumulated value of output channel o.  Kernels
+// whose stores sit inside their main loop take it as a template flag (kEp):
+// the instantiation without it has no epilogue code at all (its parameter
+// loads would otherwise make the stores wait for every load in flight).  The
+// branches are uniform (kernel arguments).
+template <bool kEp = true>
+__device__ __forceinline__ float epilogue(const ConvArgs& a, int32_t o, float v) {
+    if constexpr (!kEp) return v;
+    if (a.ep_scale && a.ep_bias) v = fmaf(v, a.ep_scale[o], a.ep_bias[o]);
+    else if (a.ep_scale) v *= a.ep_scale[o];
+    else if (a.ep_bias) v += a.ep_bias[o];
+    if (a.ep_act == ONEXN_ACT_RELU) v = fmaxf(v, 0.f);
+    else if (a.ep_act == ONEXN_ACT_RELU6) v = fminf(fmaxf(v, 0.f), 6.f);
+    return v;
+}
+
+inline bool has_epilogue(const ConvArgs& a) {
+    return a.ep_scale || a.ep_bias || a.ep_act != ONEXN_ACT_NONE;
+}
+
+// Calls f(std::true_type) when the launch has an epilogue, else
+// f(std::false_type): f instantiates the kernel with kEp accordingly.
+template <typename F>
+onexn_status with_epilogue(const ConvArgs& a, F f) {
+    if (has_epilogue(a)) return f(std::true_type{});
+    return f(std::false_type{});
+}
 
 // Physical workgroup id -> logical id such that each XCD gets a contiguous
 // range of logical ids (workgroup i runs on XCD i % 8).

@@ -113,7 +113,7 @@ __global__ void __launch_bounds__(kThreads) fma_conv(ConvArgs a) {
 #pragma unroll
         for (int o = 0; o < N; ++o) {
             const int32_t oc = g * N + o;
-            if (oc < a.n) store_out(&y[pp[i].ybase + int64_t(oc) * a.y_c], from_f32<TY>(acc[i][o]));
+            if (oc < a.n) store_out(&y[pp[i].ybase + int64_t(oc) * a.y_c], from_f32<TY>(epilogue(a, oc, acc[i][o])));
         }
     }
 }
@@ -304,7 +304,7 @@ __global__ void __launch_bounds__(kThreads) mfma_conv(ConvArgs a) {
         for (int r = 0; r < int(sizeof(acc_t) / 4); ++r) {
             const int row = (MB == 16) ? (4 * (lane / 16) + r) : (8 * (r / 4) + 4 * (lane / 32) + (r % 4));
             const int32_t oc = g * N + row;
-            if (oc < a.n) store_out(&y[op.ybase + int64_t(oc) * a.y_c], from_f32<TY>(acc[j][r]));
+            if (oc < a.n) store_out(&y[op.ybase + int64_t(oc) * a.y_c], from_f32<TY>(epilogue(a, oc, acc[j][r])));
         }
     }
 }

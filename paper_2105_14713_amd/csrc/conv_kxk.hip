@@ -44,7 +44,7 @@ constexpr int kKxThreads = 64 * kKxWaves;
 constexpr int kKxMaxRem = 9;   // staged positions per lane per channel: (virtual rows x Wp) <= 9 * 256
 constexpr int kKxSplitMaxG = 256;   // col-groups of a layer the balanced split takes
 
-template <int N, int K, int NBW, int CC, bool SPLIT>
+template <int N, int K, int NBW, int CC, bool SPLIT, bool kEp>
 __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
@@ -287,7 +287,7 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
             const int32_t oc = g * N + M::row(lane, r);
             if (oc >= a.n) continue;
             if (SPLIT && split) unsafeAtomicAdd(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
-            else store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            else store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[nb][r]));
         }
     }
     };
@@ -442,7 +442,10 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
     a.kx_tiles = int32_t(tiles);
     const size_t lds = size_t(kx_lds_bytes(CC, s.cp, N, K * K));
     // (NCHW output, contiguous and 16-byte aligned for the zero fill.)
-    const bool can_split = a.G <= kKxSplitMaxG && a.y_c == a.HWo && reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
+    // (The parts of a split block add raw sums into y, so a fused epilogue
+    // takes the unsplit kernel.)
+    const bool can_split = !has_epilogue(a) && a.G <= kKxSplitMaxG && a.y_c == a.HWo &&
+                           reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
     const int split = can_split ? kx_split_choice(s, total) : 0;
     if (split > 0) {
         const int64_t ny = int64_t(a.npix / a.HWo) * a.y_img;
@@ -453,9 +456,12 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
             return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(zerr));
         // (Ranges shorter than an eighth of a block only add partial sums.)
         a.total = int32_t(std::min<int64_t>(8 * total, int64_t(split) * device_cu_count()));
-        hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, true>), dim3(uint32_t(a.total)), dim3(kKxThreads), lds, stream, a);
+        hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, true, false>), dim3(uint32_t(a.total)), dim3(kKxThreads), lds, stream, a);
     } else {
-        hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, false>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
+        if (has_epilogue(a))
+            hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, false, true>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
+        else
+            hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, false, false>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);
     }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess)

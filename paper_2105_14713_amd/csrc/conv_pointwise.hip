@@ -58,7 +58,7 @@ struct PwShape {
     static constexpr int BLK = kPwSteps * PwMfma<N>::KS;  // BSR entries per block
 };
 
-template <int N, int WPG, bool kVec4>
+template <int N, int WPG, bool kVec4, bool kEp>
 __global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef PwShape<N, WPG> SH;
@@ -244,7 +244,7 @@ __global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
                         if (o >= a.n) continue;
                         vec_t v;
 #pragma unroll
-                        for (int e = 0; e < NB; ++e) v[e] = acc[e][r];
+                        for (int e = 0; e < NB; ++e) v[e] = onexn::epilogue<kEp>(a, o, acc[e][r]);
                         store_out(reinterpret_cast<vec_t*>(y + yb + int64_t(o) * a.y_c), v);
                     }
                 }
@@ -258,7 +258,7 @@ __global__ void __launch_bounds__(kPwThreads) pw_mfma_f32(ConvArgs a) {
 #pragma unroll
                     for (int r = 0; r < M::ACC; ++r) {
                         const int32_t o = g * N + M::row(lane, r);
-                        if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], acc[e][r]);
+                        if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], onexn::epilogue<kEp>(a, o, acc[e][r]));
                     }
                 }
             }
@@ -360,8 +360,11 @@ onexn_status launch_pw(ConvArgs a, hipStream_t s) {
     a.tile_ranges = int32_t(ranges);
     const bool vec4 = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
                       (reinterpret_cast<uintptr_t>(a.y) & 15) == 0;
-    if (vec4) return launch_grid(pw_mfma_f32<N, WPG, true>, a, ranges * gsets, s, kPwThreads);
-    return launch_grid(pw_mfma_f32<N, WPG, false>, a, ranges * gsets, s, kPwThreads);
+    return with_epilogue(a, [&](auto ep) {
+        constexpr bool E = decltype(ep)::value;
+        if (vec4) return launch_grid(pw_mfma_f32<N, WPG, true, E>, a, ranges * gsets, s, kPwThreads);
+        return launch_grid(pw_mfma_f32<N, WPG, false, E>, a, ranges * gsets, s, kPwThreads);
+    });
 }
 
 template <int N>

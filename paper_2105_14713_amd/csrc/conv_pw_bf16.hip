@@ -104,7 +104,7 @@ struct QStep {
     int32_t rz, len, smin, smax;
 };
 
-template <typename TY>
+template <typename TY, bool kEp>
 __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
     __shared__ __attribute__((aligned(16))) char sX[kQRing * kQBufB + kQRowB];
     __shared__ __attribute__((aligned(16))) char sA[kQWaves * kQRingE * kQARowB];
@@ -392,7 +392,7 @@ __global__ void __launch_bounds__(kQThreads) pw_bf16(ConvArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int32_t o = g * 32 + PwMfma<32>::row(lane, r);
-                    if (o < a.n) store_out(&yb[int64_t(o) * a.y_c], from_f32<TY>(acc[e][r]));
+                    if (o < a.n) store_out(&yb[int64_t(o) * a.y_c], from_f32<TY>(epilogue<kEp>(a, o, acc[e][r])));
                 }
             }
         }
@@ -408,7 +408,9 @@ onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     const int64_t nitems = ntiles * ((a.G + kQWaves - 1) / kQWaves);
     int64_t wgs = nitems;
     if (tuning(kTunePwbWgs) >= 1) wgs = std::min<int64_t>(tuning(kTunePwbWgs), nitems);
-    return launch_grid(pw_bf16<TY>, a, wgs, s, kQThreads);
+    return with_epilogue(a, [&](auto ep) {
+        return launch_grid(pw_bf16<TY, decltype(ep)::value>, a, wgs, s, kQThreads);
+    });
 }
 
 }  // namespace

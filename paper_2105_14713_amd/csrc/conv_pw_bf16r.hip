@@ -95,7 +95,7 @@ template <> struct Out8<float> {
 // reads per MFMA; an image's last granule then starts 8 pixels before its
 // end and its first pixels, duplicates of the previous granule's, are not
 // stored).
-template <typename TY, int kRP, int GP>
+template <typename TY, int kRP, int GP, bool kEp>
 __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     static_assert(GP == 4 || GP == 8, "granule of 4 or 8 pixels");
     typedef typename std::conditional<GP == 8, u32x4, u32x2>::type gran_t;
@@ -238,6 +238,8 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
         const int32_t o = g * 32 + PwMfma<32>::row(lane, r);
         if (o >= a.n) continue;
         TY* const yr = yb + int64_t(o) * a.y_c;
+#pragma unroll
+        for (int k = 0; k < GP; ++k) acc[k][r] = epilogue<kEp>(a, o, acc[k][r]);
         if constexpr (GP == 8) {
             const typename Out4<TY>::T lo = Out4<TY>::pack(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
             const typename Out4<TY>::T hi = Out4<TY>::pack(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
@@ -251,7 +253,7 @@ __global__ void __launch_bounds__(kRThreads) pw_bf16r(ConvArgs a) {
     }
 }
 
-template <typename TY>
+template <typename TY, bool E>
 onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     const int64_t batch = a.npix / a.HWo;
     const int64_t gsets = (a.G + kRWaves - 1) / kRWaves;
@@ -265,14 +267,14 @@ onexn_status launch_typed(ConvArgs a, hipStream_t s) {
     if (tuning(kTunePwbRp) >= 0) rp = tuning(kTunePwbRp);
     if (gp == 8 && a.HWo >= 8) {
         const int64_t grid = (batch * ((a.HWo + 7) / 8) + kRGran - 1) / kRGran * gsets;
-        if (rp == 2) return launch_grid(pw_bf16r<TY, 2, 8>, a, grid, s, kRThreads);
-        return launch_grid(pw_bf16r<TY, 1, 8>, a, grid, s, kRThreads);
+        if (rp == 2) return launch_grid(pw_bf16r<TY, 2, 8, E>, a, grid, s, kRThreads);
+        return launch_grid(pw_bf16r<TY, 1, 8, E>, a, grid, s, kRThreads);
     }
     const int64_t grid = (batch * (a.HWo / 4) + kRGran - 1) / kRGran * gsets;
     switch (rp) {
-        case 4: return launch_grid(pw_bf16r<TY, 4, 4>, a, grid, s, kRThreads);
-        case 6: return launch_grid(pw_bf16r<TY, 6, 4>, a, grid, s, kRThreads);
-        default: return launch_grid(pw_bf16r<TY, 2, 4>, a, grid, s, kRThreads);
+        case 4: return launch_grid(pw_bf16r<TY, 4, 4, E>, a, grid, s, kRThreads);
+        case 6: return launch_grid(pw_bf16r<TY, 6, 4, E>, a, grid, s, kRThreads);
+        default: return launch_grid(pw_bf16r<TY, 2, 4, E>, a, grid, s, kRThreads);
     }
 }
 
@@ -292,8 +294,11 @@ bool pw_bf16r_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn
 }
 
 onexn_status launch_pw_bf16r(ConvArgs a, onexn_dtype ydt, hipStream_t s) {
-    if (ydt == ONEXN_BF16) return launch_typed<uint16_t>(a, s);
-    return launch_typed<float>(a, s);
+    return with_epilogue(a, [&](auto ep) {
+        constexpr bool E = decltype(ep)::value;
+        if (ydt == ONEXN_BF16) return launch_typed<uint16_t, E>(a, s);
+        return launch_typed<float, E>(a, s);
+    });
 }
 
 }  // namespace onexn

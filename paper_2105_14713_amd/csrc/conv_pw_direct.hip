@@ -40,7 +40,7 @@ namespace {
 constexpr int kDThreads = 256;
 // kDB: MFMA steps per batch (8 for long contractions, 2 for short ones,
 // whose waves would otherwise multiply mostly zero padding).
-template <int N, int NB, int KSPLIT, int kDB>
+template <int N, int NB, int KSPLIT, int kDB, bool kEp>
 __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
@@ -190,7 +190,7 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
             const int32_t oc = g * N + M::row(lane, r);
-            if (oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            if (oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[nb][r]));
         }
     }
 }
@@ -206,8 +206,11 @@ onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
     const int64_t per_wave = a.G > 0 ? a.t / a.G / KSPLIT : 0;
     int kdb = per_wave < 8 * 8 * KS ? 2 : 8;
     if (tuning(kTuneDirectKdb) >= 0) kdb = tuning(kTuneDirectKdb);
-    if (kdb == 2) return launch_grid(pw_direct<N, NB, KSPLIT, 2>, a, grid, s, kDThreads);
-    return launch_grid(pw_direct<N, NB, KSPLIT, 8>, a, grid, s, kDThreads);
+    return with_epilogue(a, [&](auto ep) {
+        constexpr bool E = decltype(ep)::value;
+        if (kdb == 2) return launch_grid(pw_direct<N, NB, KSPLIT, 2, E>, a, grid, s, kDThreads);
+        return launch_grid(pw_direct<N, NB, KSPLIT, 8, E>, a, grid, s, kDThreads);
+    });
 }
 
 // (column blocks per unit, waves per unit): the largest tile that gives every

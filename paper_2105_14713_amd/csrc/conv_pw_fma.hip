@@ -37,7 +37,7 @@ constexpr int kFWin = 256;   // kept blocks per staged window (per wave)
 
 // V4: a lane owns 4 consecutive pixels (pixels per image a multiple of 4,
 // 16-byte aligned x and y), read and written with 16-byte accesses.
-template <int N, int PPT, int GSW, bool V4>
+template <int N, int PPT, int GSW, bool V4, bool kEp>
 __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     static_assert(!V4 || PPT == 4, "4 consecutive pixels per lane");
     constexpr int KSPLIT = 4 / GSW;
@@ -203,13 +203,14 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
             if (oc >= a.n) continue;
             if constexpr (V4) {
                 if (yo[0] >= 0) {
-                    const f32x4 v = {acc[o][0], acc[o][1], acc[o][2], acc[o][3]};
+                    const f32x4 v = {epilogue<kEp>(a, oc, acc[o][0]), epilogue<kEp>(a, oc, acc[o][1]),
+                                     epilogue<kEp>(a, oc, acc[o][2]), epilogue<kEp>(a, oc, acc[o][3])};
                     store_out(reinterpret_cast<f32x4*>(y + yo[0] + int64_t(oc) * a.y_c), v);
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < PPT; ++i)
-                    if (yo[i] >= 0) store_out(&y[yo[i] + int64_t(oc) * a.y_c], acc[o][i]);
+                    if (yo[i] >= 0) store_out(&y[yo[i] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[o][i]));
             }
         }
     }
@@ -228,9 +229,16 @@ onexn_status launch_cfg(ConvArgs a, hipStream_t s) {
     if constexpr (PPT == 4) {
         const bool v4 = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
                         (reinterpret_cast<uintptr_t>(a.y) & 15) == 0 && tuning(kTuneFmaNoV4) != 1;
-        if (v4) return launch_grid(pw_fma<N, PPT, GSW, true>, a, tiles * gsets, s, kFThreads);
+        if (v4)
+            return with_epilogue(a, [&](auto ep) {
+                return launch_grid(pw_fma<N, PPT, GSW, true, decltype(ep)::value>, a, tiles * gsets, s,
+                                   kFThreads);
+            });
     }
-    return launch_grid(pw_fma<N, PPT, GSW, false>, a, tiles * gsets, s, kFThreads);
+    return with_epilogue(a, [&](auto ep) {
+        return launch_grid(pw_fma<N, PPT, GSW, false, decltype(ep)::value>, a, tiles * gsets, s,
+                           kFThreads);
+    });
 }
 
 // Tile shapes (pixels per lane, col-groups per workgroup): four col-groups

@@ -60,7 +60,7 @@ __device__ __forceinline__ void lds_store(int32_t* p, int32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-template <int N, int SW, bool kVec4>
+template <int N, int SW, bool kVec4, bool kEp>
 __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
@@ -346,7 +346,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
                     if (o >= a.n) continue;
                     vec_t v;
 #pragma unroll
-                    for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, zeros ? 0.f : acc[e][r]);
+                    for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, epilogue<kEp>(a, o, zeros ? 0.f : acc[e][r]));
                     store_out(reinterpret_cast<vec_t*>(yb + int64_t(o) * a.y_c), v);
                 }
             }
@@ -360,7 +360,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 #pragma unroll
                 for (int r = 0; r < M::ACC; ++r) {
                     const int32_t o = g * N + M::row(lane, r);
-                    if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], zeros ? 0.f : acc[e][r]);
+                    if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], epilogue<kEp>(a, o, zeros ? 0.f : acc[e][r]));
                 }
             }
         }
@@ -536,8 +536,11 @@ onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
     const int64_t total = tiles * a.slices * (int64_t(a.t) + a.G);
     a.cost_q = int32_t(total / wgs);
     a.cost_r = int32_t(total % wgs);
-    if (vec4_ok(a)) return launch_grid(pw_tile_f32<N, SW, true>, a, wgs, s, kTileThreads);
-    return launch_grid(pw_tile_f32<N, SW, false>, a, wgs, s, kTileThreads);
+    return with_epilogue(a, [&](auto ep) {
+        constexpr bool E = decltype(ep)::value;
+        if (vec4_ok(a)) return launch_grid(pw_tile_f32<N, SW, true, E>, a, wgs, s, kTileThreads);
+        return launch_grid(pw_tile_f32<N, SW, false, E>, a, wgs, s, kTileThreads);
+    });
 }
 
 }  // namespace

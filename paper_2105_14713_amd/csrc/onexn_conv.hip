@@ -41,15 +41,19 @@ bool generic_forced() { return tuning(kTuneKernel) == 1; }
 
 using namespace onexn;
 
-extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev,
-                                         const void* D_dev, onexn_dtype wdt, int32_t n, int32_t m,
-                                         int32_t kh, int32_t kw, int32_t N, int64_t t,
-                                         const void* x_dev, onexn_dtype xdt, onexn_layout layout,
-                                         int32_t batch, int32_t H, int32_t W, int32_t stride_h,
-                                         int32_t stride_w, int32_t pad_h, int32_t pad_w,
-                                         void* y_dev, onexn_dtype ydt, void* stream) {
+namespace {
+
+onexn_status conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                        onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw, int32_t N,
+                        int64_t t, const void* x_dev, onexn_dtype xdt, onexn_layout layout,
+                        int32_t batch, int32_t H, int32_t W, int32_t stride_h, int32_t stride_w,
+                        int32_t pad_h, int32_t pad_w, void* y_dev, onexn_dtype ydt,
+                        const float* scale_dev, const float* bias_dev, onexn_act act,
+                        void* stream) {
     clear_error();
     if (!P_dev) return fail(ONEXN_ERR_NULL, "conv2d_fwd: NULL P");
+    if (act != ONEXN_ACT_NONE && act != ONEXN_ACT_RELU && act != ONEXN_ACT_RELU6)
+        return fail(ONEXN_ERR_ARG, "conv2d_fwd: unknown activation %d", int(act));
     if (batch != 0 && (!x_dev || !y_dev)) return fail(ONEXN_ERR_NULL, "conv2d_fwd: NULL x or y");
     if (t > 0 && (!I_dev || !D_dev)) return fail(ONEXN_ERR_NULL, "conv2d_fwd: NULL I or D with t > 0");
     if ((wdt != ONEXN_F32 && wdt != ONEXN_BF16) || (xdt != ONEXN_F32 && xdt != ONEXN_BF16) ||
@@ -101,6 +105,9 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     a.ph = pad_h;
     a.pw = pad_w;
     a.t = int32_t(t);
+    a.ep_scale = scale_dev;
+    a.ep_bias = bias_dev;
+    a.ep_act = act;
     a.npix = int32_t(int64_t(batch) * Ho * Wo);
     a.x_img = int64_t(m) * H * W;
     a.y_img = int64_t(n) * Ho * Wo;
@@ -136,6 +143,31 @@ extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     return launch_generic(a, xdt, ydt, s);
+}
+
+}  // namespace
+
+extern "C" onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev,
+                                         const void* D_dev, onexn_dtype wdt, int32_t n, int32_t m,
+                                         int32_t kh, int32_t kw, int32_t N, int64_t t,
+                                         const void* x_dev, onexn_dtype xdt, onexn_layout layout,
+                                         int32_t batch, int32_t H, int32_t W, int32_t stride_h,
+                                         int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                         void* y_dev, onexn_dtype ydt, void* stream) {
+    return conv2d_fwd(P_dev, I_dev, D_dev, wdt, n, m, kh, kw, N, t, x_dev, xdt, layout, batch, H,
+                      W, stride_h, stride_w, pad_h, pad_w, y_dev, ydt, nullptr, nullptr,
+                      ONEXN_ACT_NONE, stream);
+}
+
+extern "C" onexn_status onexn_conv2d_fwd_fused(
+    const int32_t* P_dev, const int32_t* I_dev, const void* D_dev, onexn_dtype wdt, int32_t n,
+    int32_t m, int32_t kh, int32_t kw, int32_t N, int64_t t, const void* x_dev, onexn_dtype xdt,
+    onexn_layout layout, int32_t batch, int32_t H, int32_t W, int32_t stride_h, int32_t stride_w,
+    int32_t pad_h, int32_t pad_w, void* y_dev, onexn_dtype ydt, const float* scale_dev,
+    const float* bias_dev, onexn_act act, void* stream) {
+    return conv2d_fwd(P_dev, I_dev, D_dev, wdt, n, m, kh, kw, N, t, x_dev, xdt, layout, batch, H,
+                      W, stride_h, stride_w, pad_h, pad_w, y_dev, ydt, scale_dev, bias_dev, act,
+                      stream);
 }
 
 extern "C" onexn_status onexn_set_tuning(const char* name, int32_t value) {

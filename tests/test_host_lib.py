@@ -236,3 +236,28 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros(1, 1, 2, 2)
     with pytest.raises(ValueError, match="device tensor"):
         onexn.conv2d_fwd(P, I, D, 4, x)
+
+
+def test_set_tuning_errors(lib):
+    assert lib.onexn_set_tuning(b"pw_kernel", -1) == 0
+    assert lib.onexn_set_tuning(b"no_such_knob", 1) == 2        # ONEXN_ERR_ARG
+    assert "no_such_knob" in onexn.last_error()
+    assert lib.onexn_set_tuning(None, 1) == 1                    # ONEXN_ERR_NULL
+    assert lib.onexn_set_tuning(b"kxk_split", -2) == 2
+    for name in ("kernel", "pw_kernel", "pwb_kernel", "pw_wpg", "pw_ranges", "pw_wgs", "pwb_wgs",
+                 "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw", "fma_no_v4",
+                 "fma_tile", "kxk_split", "kxk_tp"):
+        assert lib.onexn_set_tuning(name.encode(), -1) == 0, name
+
+
+def test_fused_conv_rejects_unknown_activation_before_any_launch(lib):
+    """The argument checks run on the host before anything is enqueued (batch 0:
+    nothing would be launched anyway), so this runs without a GPU."""
+    dummy = ctypes.c_int32(0)
+    p = ctypes.addressof(dummy)
+    st = lib.onexn_conv2d_fwd_fused(p, p, p, 0, 32, 8, 1, 1, 16, 1, None, 0, 0, 0, 4, 4, 1, 1, 0, 0,
+                                    None, 0, None, None, 3, None)
+    assert st == 2 and "activation" in onexn.last_error()
+    st = lib.onexn_conv2d_fwd_fused(p, p, p, 0, 32, 8, 1, 1, 16, 1, None, 0, 0, 0, 4, 4, 1, 1, 0, 0,
+                                    None, 0, None, None, 2, None)
+    assert st == 0   # batch 0 with a valid activation: a no-op

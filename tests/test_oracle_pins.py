@@ -181,6 +181,62 @@ def test_composite_permutation_invariance(oracle_lib, p):
 
 
 # ---------------------------------------------------------------------------
+# The epilogue after a convolution: folded batch norm (or bias) and ReLU/ReLU6.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("act", ["none", "relu", "relu6"])
+def test_epilogue_equals_torch_batch_norm_and_activation(oracle_lib, act):
+    """Inference batch norm (torch's routine, fp64) folds into scale = gamma /
+    sqrt(var + eps) and bias = beta - mean * scale; the oracle's per-channel
+    affine map plus activation must give torch's batch_norm + relu/relu6."""
+    gen = torch.Generator().manual_seed(21)
+    y = torch.randn((3, 7, 5, 4), generator=gen, dtype=torch.float64) * 4
+    gamma = torch.randn(7, generator=gen, dtype=torch.float64)
+    beta = torch.randn(7, generator=gen, dtype=torch.float64)
+    mean = torch.randn(7, generator=gen, dtype=torch.float64)
+    var = torch.rand(7, generator=gen, dtype=torch.float64) + 0.5
+    eps = 1e-5
+    ref = torch.nn.functional.batch_norm(y, mean, var, gamma, beta, False, 0.0, eps)
+    ref = {"none": ref, "relu": torch.relu(ref), "relu6": torch.nn.functional.relu6(ref)}[act]
+    scale = gamma / torch.sqrt(var + eps)
+    bias = beta - mean * scale
+    got = oracle_lib.epilogue(y.numpy(), scale.numpy(), bias.numpy(), act)
+    np.testing.assert_allclose(got, ref.numpy(), rtol=1e-13, atol=1e-13)
+    # Either parameter absent: scale 1 / bias 0.
+    np.testing.assert_array_equal(oracle_lib.epilogue(y.numpy(), None, bias.numpy()),
+                                  (y + bias[None, :, None, None]).numpy())
+    np.testing.assert_array_equal(oracle_lib.epilogue(y.numpy(), scale.numpy(), None),
+                                  (y * scale[None, :, None, None]).numpy())
+    np.testing.assert_array_equal(oracle_lib.epilogue(y.numpy()), y.numpy())
+
+
+def test_composite_with_epilogue_permutation_invariance(oracle_lib):
+    """Sec. 3.3: with layer 1's filters rearranged, its per-channel scale and
+    bias taken in the same order and layer 2's input channels permuted, the
+    two-layer network (conv -> folded BN -> ReLU6 -> pruned conv) is unchanged."""
+    gen = torch.Generator().manual_seed(8)
+    w1 = torch.randint(-3, 4, (16, 6, 3, 3), generator=gen).double().numpy()
+    w2 = torch.randint(-2, 3, (12, 16, 1, 1), generator=gen).double().numpy()
+    x = torch.randint(0, 4, (2, 6, 7, 9), generator=gen).double().numpy()
+    scale = torch.randint(-2, 3, (16,), generator=gen).double().numpy()
+    bias = torch.randint(-9, 10, (16,), generator=gen).double().numpy()
+    pr1 = oracle_lib.prune(w1, 4, 0.5, rearrange=True)
+    assert not np.array_equal(pr1.perm, np.arange(16))
+    pr2 = oracle_lib.prune(w2[:, pr1.perm], 4, 0.5, rearrange=False)
+    h = oracle_lib.epilogue(oracle_lib.conv2d(x, pr1.wbar, (1, 1), (1, 1)), scale[pr1.perm],
+                            bias[pr1.perm], "relu6")
+    y_re = oracle_lib.conv2d(h, pr2.wbar, (1, 1), (0, 0))
+    # The same network in the original channel order, through torch's conv.
+    w1o = np.empty_like(pr1.wbar)
+    w1o[pr1.perm] = pr1.wbar
+    w2o = np.empty_like(pr2.wbar)
+    w2o[:, pr1.perm] = pr2.wbar
+    ho = torch_conv64(x, w1o, 1, 1) * scale[None, :, None, None] + bias[None, :, None, None]
+    ho = np.clip(ho, 0.0, 6.0)
+    np.testing.assert_array_equal(y_re, torch_conv64(ho, w2o, 1, 0))
+
+
+# ---------------------------------------------------------------------------
 # Closed forms for the l1 scores and the rearrangement.
 # ---------------------------------------------------------------------------
 
