@@ -34,7 +34,6 @@ struct ConvArgs {
     int64_t y_img;      // elements per output image
     int32_t y_c, y_pix;
     int32_t total;      // workgroups in the grid
-    int32_t tile_ranges;   // streamed pointwise kernel: pixel-tile ranges per col-group set
     int32_t slices;        // resident-tile pointwise kernel: slices per pixel tile,
     int32_t cost_q, cost_r;   // and its total work cost divided by the grid (quotient, remainder)
     int32_t kx_rows;       // k x k staged kernel: output rows per tile,
@@ -202,12 +201,8 @@ int device_cu_count();
 
 // Kernel families (each defined in its own translation unit).
 onexn_status launch_generic(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
-bool pointwise_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
-onexn_status launch_pointwise(ConvArgs a, onexn_dtype xdt, onexn_dtype ydt, hipStream_t stream);
 bool pw_tile_applies(const ConvArgs& a);
 onexn_status launch_pw_tile(ConvArgs a, hipStream_t stream);
-bool pw_bf16_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
-onexn_status launch_pw_bf16(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
 bool pw_bf16r_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 onexn_status launch_pw_bf16r(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
 bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);

@@ -546,6 +546,8 @@ onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
 }  // namespace
 
 bool pw_tile_applies(const ConvArgs& a) {
+    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
+    if (a.y_c != a.HWo || a.x_c != a.H * a.W) return false;   // NCHW
     return (a.N == 16 || a.N == 32) && tile_shape(a).sw > 0;
 }
 

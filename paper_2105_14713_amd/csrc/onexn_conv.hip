@@ -26,9 +26,8 @@ namespace {
 // Stored as value + 1, so that the zero-initialised array reads kTuneAuto.
 std::atomic<int32_t> g_tuning[kTuneCount];
 const char* const kTuneNames[kTuneCount] = {
-    "kernel", "pw_kernel", "pwb_kernel", "pw_wpg", "pw_ranges", "pw_wgs", "pwb_wgs", "pwb_gp",
-    "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split",
-    "kxk_tp"};
+    "kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw",
+    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp"};
 
 }  // namespace
 
@@ -125,21 +124,24 @@ onexn_status conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* 
         a.y_pix = n;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (pw_bf16r_applies(a, xdt, ydt, layout) && tuning(kTunePwbKernel) != 1) return launch_pw_bf16r(a, ydt, s);
-    if (pw_bf16_applies(a, xdt, ydt, layout)) return launch_pw_bf16(a, ydt, s);
-    // fp32 1x1 layers: the LDS-tile pointwise kernels for layers that widen
-    // the channels over many pixels, the register-operand kernel for the
-    // rest (contractions at least as long as the output is wide, few pixels,
-    // any stride or padding).  The pw_kernel tuning overrides the choice.
+    if (pw_bf16r_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_bf16r(a, ydt, s);
+    // fp32 1x1 layers: the resident-tile kernel for stride-1 layers that
+    // widen the channels over many pixels, the register-operand kernel for
+    // the rest (contractions at least as long as the output is wide, few
+    // pixels, any stride or padding).  The pw_kernel tuning overrides the
+    // choice (1: resident tile, an error where it does not fit; 3: register
+    // operands).
     const bool direct = pw_direct_applies(a, xdt, ydt, layout) && !generic_forced();
-    if (pointwise_applies(a, xdt, ydt, layout)) {
+    if (direct) {
         const int32_t pwk = tuning(kTunePwKernel);
-        const bool forced_pw = pwk == 1 || pwk == 2;
         const bool prefer_direct = pwk == 3 || a.m >= a.n || a.npix <= 8192 ||
                                    (a.N == 32 && a.npix <= 32768 && a.m <= 128);
-        if (!direct || forced_pw || !prefer_direct) return launch_pointwise(a, xdt, ydt, s);
+        const bool tile = pw_tile_applies(a);
+        if (pwk == 1 && !tile && a.kh == 1 && a.kw == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0)
+            return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: the resident-tile kernel does not fit this layer");
+        if (tile && (pwk == 1 || !prefer_direct)) return launch_pw_tile(a, s);
+        return launch_pw_direct(a, s);
     }
-    if (direct) return launch_pw_direct(a, s);
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     return launch_generic(a, xdt, ydt, s);

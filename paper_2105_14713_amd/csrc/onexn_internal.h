@@ -20,12 +20,8 @@ void clear_error();
 // the dispatch rules.
 enum Tune : int {
     kTuneKernel,       // 1: the generic gather kernels for every layer
-    kTunePwKernel,     // 1x1 fp32 N = 16/32: 1 resident tile, 2 streamed, 3 register-operand
-    kTunePwbKernel,    // 1x1 bf16 N = 32: 1 the LDS-queue kernel
-    kTunePwWpg,        // streamed 1x1: waves per col-group (1, 2, 4, 8)
-    kTunePwRanges,     // streamed 1x1: pixel-tile ranges per col-group set
+    kTunePwKernel,     // 1x1 fp32 N = 16/32: 1 resident tile, 3 register-operand
     kTunePwWgs,        // resident-tile 1x1: workgroups
-    kTunePwbWgs,       // LDS-queue bf16: workgroups
     kTunePwbGp,        // register-gathered bf16: pixels per granule (4, 8)
     kTunePwbRp,        // register-gathered bf16: steps in flight
     kTuneDirectKdb,    // register-operand 1x1: MFMA steps per batch (2, 8)

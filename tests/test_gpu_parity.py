@@ -284,26 +284,6 @@ def test_config3_mobilenet_v2_layer_sampled(li):
             assert rel_err(got, ref) <= 1e-5, (base.name, N, p)
 
 
-@pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
-@pytest.mark.parametrize("wpg", ["1", "2", "4", "8"])
-@pytest.mark.parametrize("N", [16, 32])
-def test_pointwise_variants_integer_exact(N, wpg, hw, tune):
-    """Every waves-per-col-group variant of the streamed pointwise kernel:
-    several channel chunks with a ragged last one (m = 300 > the largest
-    chunk), col-group sets with a partial last set and a ragged last
-    col-group, and p from dense to nearly empty (col-groups with no entries in
-    some chunks)."""
-    tune("pw_kernel", 2)
-    tune("pw_wpg", wpg)
-    n = 9 * N + N // 2
-    w, x = workloads.gen_integer_layer(seed=N, cout=n, cin=300, k=1, batch=2, H=hw[0], W=hw[1],
-                                       wmax=1, xmax=2)
-    for p in (0.0, 0.5, 0.95):
-        y, _ = gpu_conv(w, x, N, p, True, 1, 0)
-        ref, _ = oracle_conv(w, x, N, p, True, 1, 0)
-        np.testing.assert_array_equal(y, ref)
-
-
 @pytest.mark.parametrize("wgs", ["1", "5", "default"])
 @pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
 @pytest.mark.parametrize("N,groups,m", [
@@ -336,7 +316,7 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, tune):
         np.testing.assert_array_equal(y, ref)
 
 
-@pytest.mark.parametrize("variant", ["g4rp2", "g4rp4", "g4rp6", "g8rp1", "g8rp2", "queue1", "queue7", "queue"])
+@pytest.mark.parametrize("variant", ["g4rp2", "g4rp4", "g4rp6", "g8rp1", "g8rp2"])
 @pytest.mark.parametrize("shape", [
     dict(m=300, B=3, H=14, W=14),    # 5 channel chunks (ragged last), partial last granule per image
     dict(m=64, B=2, H=12, W=12),     # one chunk, whole granules, tiles across images
@@ -345,24 +325,17 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, tune):
     dict(m=2100, B=1, H=4, W=4),     # more input channels than the register kernel stages
 ], ids=["m300", "m64", "m45", "m700", "m2100"])
 def test_pw_bf16_integer_exact(shape, variant, tune):
-    """The bf16 pointwise kernels (1x1, N = 32, pixels per image a multiple of
+    """The bf16 pointwise kernel (1x1, N = 32, pixels per image a multiple of
     4): the register-gathered kernel with 4-pixel granules at pipeline depths
     2, 4, 6 and with 8-pixel granules at depths 1, 2 (images of 12 and 196
-    pixels end in a half-duplicate granule), and the LDS-queue kernel at 1, 7
-    and the default number of workgroups.  Small
-    integers are exact in bf16 and in fp32 accumulation, so fp32 output is
-    bit-exact and bf16 output equals the oracle rounded to bf16.  Covers
-    ragged col-groups and a partial last set of 8 col-groups (n = 304), dense
-    to nearly empty col-groups (p = 0, 0.5, 0.97: for the queue kernel, steps
-    cut short where 16 kept channels span more chunks than LDS holds), and
-    workgroup counts that give each workgroup several work items."""
-    if variant.startswith("g"):
-        tune("pwb_gp", variant[1])
-        tune("pwb_rp", variant[4:])
-    else:
-        tune("pwb_kernel", 1)
-        if variant != "queue":
-            tune("pwb_wgs", variant[5:])
+    pixels end in a half-duplicate granule); more input channels than it
+    stages (m = 2100) take the generic kernel.  Small integers are exact in
+    bf16 and in fp32 accumulation, so fp32 output is bit-exact and bf16 output
+    equals the oracle rounded to bf16.  Covers ragged col-groups and a partial
+    last set of 8 col-groups (n = 304) and dense to nearly empty col-groups
+    (p = 0, 0.5, 0.97)."""
+    tune("pwb_gp", variant[1])
+    tune("pwb_rp", variant[4:])
     c = shape
     n = 9 * 32 + 16
     w, x = workloads.gen_integer_layer(seed=c["m"] + int(c["B"]), cout=n, cin=c["m"], k=1,
@@ -443,17 +416,17 @@ def test_kxk_matches_generic_on_random_fp32():
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "stream", "bf16", "generic", "fma", "pwfma", "direct"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "generic", "fma", "pwfma", "direct"])
 def test_reads_stay_inside_I_and_D(kind, tune):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
     t would put NaN into the output."""
     k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
-                      "stream": (1, 32, 300, torch.float32, 12), "bf16": (1, 32, 96, torch.bfloat16, 12),
+                      "bf16": (1, 32, 96, torch.bfloat16, 12),
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
                       "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
-    if kind in ("tile", "stream", "direct"):
-        tune("pw_kernel", {"tile": 1, "stream": 2, "direct": 3}[kind])
+    if kind in ("tile", "direct"):
+        tune("pw_kernel", {"tile": 1, "direct": 3}[kind])
     n = 3 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=7, cout=n, cin=m, k=k, batch=2, H=H, wmax=2, xmax=2)
     w, x = w.to(dt), x.to(dt)

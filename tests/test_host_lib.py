@@ -242,11 +242,11 @@ def test_set_tuning_errors(lib):
     assert lib.onexn_set_tuning(b"pw_kernel", -1) == 0
     assert lib.onexn_set_tuning(b"no_such_knob", 1) == 2        # ONEXN_ERR_ARG
     assert "no_such_knob" in onexn.last_error()
+    assert lib.onexn_set_tuning(b"pw_wpg", 1) == 2              # the streamed kernel's knob is gone
     assert lib.onexn_set_tuning(None, 1) == 1                    # ONEXN_ERR_NULL
     assert lib.onexn_set_tuning(b"kxk_split", -2) == 2
-    for name in ("kernel", "pw_kernel", "pwb_kernel", "pw_wpg", "pw_ranges", "pw_wgs", "pwb_wgs",
-                 "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw", "fma_no_v4",
-                 "fma_tile", "kxk_split", "kxk_tp"):
+    for name in ("kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile",
+                 "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp"):
         assert lib.onexn_set_tuning(name.encode(), -1) == 0, name
 
 
