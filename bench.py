@@ -57,6 +57,9 @@ WORKLOADS = {
 for _N in (4, 8, 16, 32):
     for _p in (0.3, 0.5, 0.7):
         WORKLOADS[f"c3_n{_N}_p{int(_p * 100)}"] = (lambda N=_N, p=_p: workloads.config3(N, p))
+for _N in (4, 32):
+    for _lay in ("rows", "cols"):
+        WORKLOADS[f"fc_n{_N}_{_lay}"] = (lambda N=_N, lay=_lay: workloads.fc_resnet50(N, lay))
 
 _ESIZE = {"f32": 4, "bf16": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -135,6 +138,9 @@ def parity_gate(prepared, wl):
         call0()
         torch.cuda.synchronize()
         y = ys[0]
+        if wl.fc_layout == "cols":        # [n][batch] -> [batch][n]
+            y = y.t().contiguous()
+        y = y.reshape(x_cpu.shape[0], layer.cout, layer.Ho, layer.Ho)
         idx = workloads.sample_outputs(tuple(y.shape), layer.N, PARITY_SAMPLES, seed=li)
         got = y.reshape(-1)[torch.from_numpy(idx).to(y.device)].double().cpu().numpy()
         pr = oracle.prune(w_cpu.double().numpy(), layer.N, layer.p, layer.rearrange)
@@ -257,15 +263,27 @@ def main():
                      "cout": layer.cout, "H": layer.H, "N": layer.N, "p": layer.p, "t": packed.t,
                      "gflop_act": fa / 1e9, "mb_alg": bb / 1e6,
                      "bound": "mfma" if t_c >= t_m else "hbm", "t_roof_us": max(t_c, t_m) * 1e6})
-        xd = x.to(dev)
         Ho = layer.Ho
         copies = max(1, math.ceil(ROTATE_BYTES / max(bb, 1)))
         copies = min(copies, 16)
+        if wl.fc_layout:
+            # A fully connected layer: x [batch][m] ("rows") or [m][batch] ("cols").
+            x2 = x.reshape(batch, layer.cin)
+            xd = (x2 if wl.fc_layout == "rows" else x2.t().contiguous()).to(dev)
+            yshape = (batch, layer.cout) if wl.fc_layout == "rows" else (layer.cout, batch)
+        else:
+            xd = x.to(dev)
+            yshape = (batch, layer.cout, Ho, Ho)
         xs = [xd] + [xd.clone() for _ in range(copies - 1)]
-        ys = [torch.empty((batch, layer.cout, Ho, Ho), dtype=odt, device=dev) for _ in range(copies)]
-        calls = [onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
-                                 layer.stride, layer.pad, "nchw", stream.cuda_stream)
-                 for r in range(copies)]
+        ys = [torch.empty(yshape, dtype=odt, device=dev) for _ in range(copies)]
+        if wl.fc_layout:
+            calls = [(lambda r=r: onexn.fc_fwd(packed.P, packed.I, packed.D, packed.n, xs[r],
+                                               wl.fc_layout, odt, ys[r], stream.cuda_stream))
+                     for r in range(copies)]
+        else:
+            calls = [onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
+                                     layer.stride, layer.pad, "nchw", stream.cuda_stream)
+                     for r in range(copies)]
         prepared.append((layer, packed, xs, ys, w, x, calls))
 
     # Parity before timing: the same bound calls the timed steps issue.
@@ -379,7 +397,8 @@ def main():
         "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.description, "batch": batch,
-                   "layers": len(wl.layers), "out_dtype": wl.out_dtype, "layout": "nchw"},
+                   "layers": len(wl.layers), "out_dtype": wl.out_dtype,
+                   "layout": wl.fc_layout or "nchw"},
         "dense_equiv_tflops": round(f_dense * args.steps / (total_ms / 1e3) / 1e12, 3),
         "hbm_gbps": round(b_alg * args.steps / (total_ms / 1e3) / 1e9, 1),
         "kernel_us": {"mean": round(avg_step_ms * 1e3, 2), "p10": round(per_step[len(per_step) // 10] * 1e3, 2),

@@ -160,6 +160,28 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
                                     void* stream);
 
 /*
+ * Fully connected layer (device, asynchronous): Sec. 3.1 treats an FC layer
+ * as the kh = kw = 1 case, so its weight [n][m] is packed like a 1x1 conv
+ * (onexn_build_mask / onexn_pack with kh = kw = 1) and
+ *   Y[b][gN .. gN+N-1] = sum_{z=P[g]}^{P[g+1]-1} X[b][I[z]] * D[z]   (Eq. 8)
+ * for every sample b and col-group g; output features in rearranged order.
+ *
+ * layout: ONEXN_NHWC: x_dev is [batch][m] (one row per sample), y_dev
+ *         [batch][n];  ONEXN_NCHW: x_dev is [m][batch] (one row per feature,
+ *         the samples contiguous), y_dev [n][batch] -- the layout in which
+ *         every gathered row is read with coalesced loads.
+ * D_dev: [t][N] (the [t][N][1][1] of onexn_pack).  scale_dev, bias_dev, act:
+ *         the fused epilogue of onexn_conv2d_fwd_fused (NULL, NULL,
+ *         ONEXN_ACT_NONE for none).  dtypes, errors and ownership as for the
+ *         convolution.
+ */
+onexn_status onexn_fc_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                          onexn_dtype wdt, int32_t n, int32_t m, int32_t N, int64_t t,
+                          const void* x_dev, onexn_dtype xdt, onexn_layout layout, int32_t batch,
+                          void* y_dev, onexn_dtype ydt, const float* scale_dev,
+                          const float* bias_dev, onexn_act act, void* stream);
+
+/*
  * Kernel-choice and launch-shape overrides (host, process-wide).
  *
  * Not part of the method: these let a caller reach a particular kernel variant

@@ -27,7 +27,7 @@ F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 
 EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
-            "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
+            "onexn_fc_fwd", "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
 ACTS = {"none": 0, "relu": 1, "relu6": 2}
 
 _lib = None
@@ -64,6 +64,10 @@ def load_library():
                                            [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
                                            [c_vp, ctypes.c_int, c_vp, c_vp, ctypes.c_int, c_vp])
     lib.onexn_conv2d_fwd_fused.restype = ctypes.c_int
+    lib.onexn_fc_fwd.argtypes = ([c_vp, c_vp, c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i64, c_vp,
+                                  ctypes.c_int, ctypes.c_int, c_i32, c_vp, ctypes.c_int, c_vp, c_vp,
+                                  ctypes.c_int, c_vp])
+    lib.onexn_fc_fwd.restype = ctypes.c_int
     lib.onexn_set_tuning.argtypes = [ctypes.c_char_p, c_i32]
     lib.onexn_set_tuning.restype = ctypes.c_int
     lib.onexn_status_string.argtypes = [ctypes.c_int]
@@ -209,6 +213,43 @@ def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: tor
     return out
 
 
+def fc_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
+           layout: str = "rows", out_dtype: Optional[torch.dtype] = None,
+           out: Optional[torch.Tensor] = None, stream: Optional[int] = None,
+           scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
+           act: str = "none") -> torch.Tensor:
+    """``onexn_fc_fwd``: x is [B][m] ("rows", one row per sample) or [m][B]
+    ("cols", one row per feature); returns y [B][n] or [n][B] (rearranged
+    feature order).  D is [t][N] or [t][N][1][1]."""
+    for name, tns in (("P", P), ("I", I), ("D", D), ("x", x)):
+        if tns.device.type != "cuda":
+            raise ValueError(f"{name} must be a device tensor")
+        if not tns.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if x.dim() != 2 or D.dim() not in (2, 4) or (D.dim() == 4 and tuple(D.shape[2:]) != (1, 1)):
+        raise ValueError("x must be 2-D and D [t][N] (or [t][N][1][1])")
+    t, N = int(D.shape[0]), int(D.shape[1])
+    if t != I.numel():
+        raise ValueError("D and I disagree on t")
+    lay = {"rows": NHWC, "cols": NCHW}[layout]
+    B, m = (x.shape[0], x.shape[1]) if layout == "rows" else (x.shape[1], x.shape[0])
+    odt = x.dtype if out_dtype is None else out_dtype
+    shape = (B, n) if layout == "rows" else (n, B)
+    if out is None:
+        out = torch.empty(shape, dtype=odt, device=x.device)
+    elif tuple(out.shape) != shape or out.dtype != odt or not out.is_contiguous():
+        raise ValueError("out has the wrong shape, dtype or layout")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device).cuda_stream
+    sp, bp, ac, _ = _epilogue_args(int(n), scale, bias, act)
+    st = load_library().onexn_fc_fwd(P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0,
+                                     _dtype_code(D.dtype), int(n), int(m), N, t, x.data_ptr(),
+                                     _dtype_code(x.dtype), lay, int(B), out.data_ptr(),
+                                     _dtype_code(odt), sp, bp, ac, stream)
+    _check(st, "onexn_fc_fwd")
+    return out
+
+
 class BoundConv:
     """A conv2d_fwd call with its arguments marshalled once; calling it
     re-issues the same launch (same tensors, same stream).  The tensors must
@@ -277,6 +318,6 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
     return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
 
 
-__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
+__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "fc_fwd", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
            "prepare_layer", "set_tuning", "status_string"]

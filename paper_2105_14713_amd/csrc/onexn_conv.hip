@@ -184,3 +184,25 @@ extern "C" onexn_status onexn_set_tuning(const char* name, int32_t value) {
         }
     return fail(ONEXN_ERR_ARG, "set_tuning: unknown name \"%s\"", name);
 }
+
+extern "C" onexn_status onexn_fc_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                                     onexn_dtype wdt, int32_t n, int32_t m, int32_t N, int64_t t,
+                                     const void* x_dev, onexn_dtype xdt, onexn_layout layout,
+                                     int32_t batch, void* y_dev, onexn_dtype ydt,
+                                     const float* scale_dev, const float* bias_dev, onexn_act act,
+                                     void* stream) {
+    clear_error();
+    if (layout != ONEXN_NCHW && layout != ONEXN_NHWC)
+        return fail(ONEXN_ERR_ARG, "fc_fwd: unknown layout %d", int(layout));
+    if (batch < 0) return fail(ONEXN_ERR_ARG, "fc_fwd: batch must be >= 0");
+    // [batch][m] rows: batch one-pixel images.  [m][batch] columns: one image
+    // of batch pixels, so the 1x1 kernels read each feature's row coalesced.
+    if (layout == ONEXN_NHWC)
+        return conv2d_fwd(P_dev, I_dev, D_dev, wdt, n, m, 1, 1, N, t, x_dev, xdt, ONEXN_NCHW, batch,
+                          1, 1, 1, 1, 0, 0, y_dev, ydt, scale_dev, bias_dev, act, stream);
+    if (batch == 0) return conv2d_fwd(P_dev, I_dev, D_dev, wdt, n, m, 1, 1, N, t, x_dev, xdt,
+                                      ONEXN_NCHW, 0, 1, 1, 1, 1, 0, 0, y_dev, ydt, scale_dev,
+                                      bias_dev, act, stream);
+    return conv2d_fwd(P_dev, I_dev, D_dev, wdt, n, m, 1, 1, N, t, x_dev, xdt, ONEXN_NCHW, 1, 1,
+                      batch, 1, 1, 0, 0, y_dev, ydt, scale_dev, bias_dev, act, stream);
+}

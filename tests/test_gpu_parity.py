@@ -405,6 +405,26 @@ def test_kxk_balanced_split_integer_exact(case, split, tune):
         np.testing.assert_array_equal(y, ref)
 
 
+@pytest.mark.parametrize("split", ["1", "4"])
+def test_kxk_balanced_split_random_fp32(split, tune):
+    """Random fp32 data with blocks much longer than the split's ranges (cut
+    into up to eight parts that add into the output in arrival order):
+    every launch is within 1e-5 of the oracle, and repeated launches agree to
+    the order-of-summation error."""
+    tune("kxk_split", split)
+    tune("kxk_tp", 128)
+    gen = torch.Generator().manual_seed(23)
+    w = workloads.gen_weight(gen, 80, 256, 3)
+    x = workloads.gen_activation(gen, (2, 256, 14, 14))
+    layer = onexn.prepare_layer(w, 32, 0.5, False)
+    xd = x.cuda()
+    ys = [layer.forward(xd, 1, 1).double().cpu().numpy() for _ in range(5)]
+    ref, _ = oracle_conv(w, x, 32, 0.5, False, 1, 1)
+    for y in ys:
+        assert rel_err(y, ref) <= 1e-5
+        assert rel_err(y, ys[0]) <= 1e-6
+
+
 def test_kxk_matches_generic_on_random_fp32():
     """Random-valued fp32 3x3 layer: the staged kernel and the oracle agree to
     1e-5 of max |y| over a contraction of 288 * 9 entries."""

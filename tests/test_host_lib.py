@@ -261,3 +261,4 @@ def test_fused_conv_rejects_unknown_activation_before_any_launch(lib):
     st = lib.onexn_conv2d_fwd_fused(p, p, p, 0, 32, 8, 1, 1, 16, 1, None, 0, 0, 0, 4, 4, 1, 1, 0, 0,
                                     None, 0, None, None, 2, None)
     assert st == 0   # batch 0 with a valid activation: a no-op
+

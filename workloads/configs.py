@@ -39,6 +39,7 @@ class Workload:
     out_dtype: str                # "f32" or "bf16" for Y
     layers: Tuple[ConvLayer, ...] = field(default_factory=tuple)
     description: str = ""
+    fc_layout: str = ""           # "rows" / "cols" for a fully connected layer, "" for convs
 
 
 def config0() -> Workload:
@@ -129,10 +130,24 @@ def config4(out_dtype: str = "bf16") -> Workload:
                     "N=32, p=0.7")
 
 
+def fc_resnet50(N: int = 32, layout: str = "rows") -> Workload:
+    """The classifier of ResNet-50 as a 1xN-pruned FC layer (Sec. 3.1: the
+    kh = kw = 1 case): 2048 -> 1000 at batch 256, fp32, p = 0.5.  1000 is not
+    a multiple of 32, so at N = 32 the last col-group is ragged.  `layout`:
+    "rows" ([batch][2048]) or "cols" ([2048][batch])."""
+    layer = ConvLayer("fc_2048_1000", 2048, 1000, 1, 1, 0, 1, N=N, p=0.5, rearrange=False,
+                      seed=5000 + N)
+    return Workload(f"fc_b256_2048x1000_n{N}_p50_f32_{layout}", 256, "f32", "f32", (layer,),
+                    f"ResNet-50 classifier as an FC layer, batch 256, 2048->1000, fp32, N={N}, "
+                    f"p=0.5, input [{'batch][2048' if layout == 'rows' else '2048][batch'}]",
+                    fc_layout=layout)
+
+
 def all_workloads() -> List[Workload]:
     out = [config0(), config1(), config2()]
     for N in (4, 8, 16, 32):
         for p in (0.3, 0.5, 0.7):
             out.append(config3(N, p))
     out += [config4("bf16"), config4("f32")]
+    out += [fc_resnet50(N, lay) for N in (4, 32) for lay in ("rows", "cols")]
     return out
