@@ -168,15 +168,9 @@ def _epilogue_args(n, scale, bias, act):
             ACTS[act], fused)
 
 
-def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
-               stride=1, pad=0, layout: str = "nchw", out_dtype: Optional[torch.dtype] = None,
-               out: Optional[torch.Tensor] = None, stream: Optional[int] = None,
-               scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
-               act: str = "none") -> torch.Tensor:
-    """``onexn_conv2d_fwd`` on device tensors; enqueued on ``stream`` (default:
-    torch's current stream), no synchronisation.  Returns y (rearranged channel order).
-    With ``scale``, ``bias`` (fp32 [n], rearranged channel order) or ``act``
-    ("relu", "relu6") it calls ``onexn_conv2d_fwd_fused``: y = act(scale * acc + bias)."""
+def _conv_call(P, I, D, n, x, stride, pad, layout, out_dtype, out, stream, scale, bias, act):
+    """Validates a conv2d_fwd call and marshals its arguments: returns (library
+    function, argument tuple, out).  Nothing is launched."""
     for name, tns in (("P", P), ("I", I), ("D", D), ("x", x)):
         if tns.device.type != "cuda":
             raise ValueError(f"{name} must be a device tensor (the convolution only runs on the GPU)")
@@ -206,10 +200,24 @@ def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: tor
     args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype),
             int(n), m, kh, kw, N, t, x.data_ptr(), _dtype_code(x.dtype), lay, B, H, W, stride[0],
             stride[1], pad[0], pad[1], out.data_ptr(), _dtype_code(odt))
+    lib = load_library()
     if fused:
-        _check(load_library().onexn_conv2d_fwd_fused(*args, sp, bp, ac, stream), "onexn_conv2d_fwd_fused")
-    else:
-        _check(load_library().onexn_conv2d_fwd(*args, stream), "onexn_conv2d_fwd")
+        return lib.onexn_conv2d_fwd_fused, args + (sp, bp, ac, stream), out
+    return lib.onexn_conv2d_fwd, args + (stream,), out
+
+
+def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
+               stride=1, pad=0, layout: str = "nchw", out_dtype: Optional[torch.dtype] = None,
+               out: Optional[torch.Tensor] = None, stream: Optional[int] = None,
+               scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
+               act: str = "none") -> torch.Tensor:
+    """``onexn_conv2d_fwd`` on device tensors; enqueued on ``stream`` (default:
+    torch's current stream), no synchronisation.  Returns y (rearranged channel order).
+    With ``scale``, ``bias`` (fp32 [n], rearranged channel order) or ``act``
+    ("relu", "relu6") it calls ``onexn_conv2d_fwd_fused``: y = act(scale * acc + bias)."""
+    fn, args, out = _conv_call(P, I, D, n, x, stride, pad, layout, out_dtype, out, stream, scale,
+                               bias, act)
+    _check(fn(*args), fn.__name__)
     return out
 
 
@@ -251,37 +259,20 @@ def fc_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.T
 
 
 class BoundConv:
-    """A conv2d_fwd call with its arguments marshalled once; calling it
-    re-issues the same launch (same tensors, same stream).  The tensors must
+    """A conv2d_fwd call with its arguments validated and marshalled once;
+    calling it issues the launch (same tensors, same stream).  The tensors must
     stay alive and unmoved while this object is used."""
 
     def __init__(self, P, I, D, n, x, out, stride=1, pad=0, layout="nchw", stream=None,
                  scale=None, bias=None, act="none"):
-        conv2d_fwd(P, I, D, n, x, stride, pad, layout, out.dtype, out, stream, scale, bias,
-                   act)   # validates
-        t, N, kh, kw = D.shape
-        lay = {"nchw": NCHW, "nhwc": NHWC}[layout]
-        B, m, H, W = x.shape if lay == NCHW else (x.shape[0], x.shape[3], x.shape[1], x.shape[2])
-        stride, pad = _pair(stride), _pair(pad)
-        if stream is None:
-            stream = torch.cuda.current_stream(x.device).cuda_stream
+        self._fn, self._args, _ = _conv_call(P, I, D, n, x, stride, pad, layout, out.dtype, out,
+                                             stream, scale, bias, act)
         self._keep = (P, I, D, x, out, scale, bias)
-        sp, bp, ac, fused = _epilogue_args(int(n), scale, bias, act)
-        self._args = (P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0,
-                      _dtype_code(D.dtype), int(n), m, kh, kw, N, t, x.data_ptr(),
-                      _dtype_code(x.dtype), lay, B, H, W, stride[0], stride[1], pad[0], pad[1],
-                      out.data_ptr(), _dtype_code(out.dtype))
-        if fused:
-            self._fn = load_library().onexn_conv2d_fwd_fused
-            self._args += (sp, bp, ac, stream)
-        else:
-            self._fn = load_library().onexn_conv2d_fwd
-            self._args += (stream,)
 
     def __call__(self):
         st = self._fn(*self._args)
         if st != ONEXN_OK:
-            _check(st, "onexn_conv2d_fwd")
+            _check(st, self._fn.__name__)
 
 
 @dataclass
