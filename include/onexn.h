@@ -24,6 +24,7 @@
 #ifndef ONEXN_H
 #define ONEXN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -73,6 +74,38 @@ typedef enum { ONEXN_ACT_NONE = 0, ONEXN_ACT_RELU = 1, ONEXN_ACT_RELU6 = 2 } one
 onexn_status onexn_build_mask(const void* w, onexn_dtype wdt, int32_t n, int32_t m, int32_t kh,
                               int32_t kw, int32_t N, double p, int32_t rearrange, int32_t* perm,
                               uint8_t* mask, int64_t* t);
+
+/*
+ * Mask building on the GPU (device, asynchronous): the same three steps as
+ * onexn_build_mask (Sec. 3.3 filter rearrangement, Sec. 3.2 / Eq. 4-5 block
+ * l1 scores, Eq. 1 / Sec. 4.1 per-layer top-(1-p) selection), for weights
+ * already on the device.  perm and mask equal onexn_build_mask's bit for bit
+ * (the same fp64 sums in the same order and the same tie rules).
+ *
+ * w_dev:    device [n][m][kh][kw] in wdt.
+ * perm_dev: out, device int32[n];  mask_dev: out, device uint8[m][G] (every
+ *           byte written).
+ * t:        out, HOST int64: the kept count, set before the call returns
+ *           (it depends only on m * G and p).
+ * workspace_dev, workspace_bytes: device scratch of at least
+ *           onexn_mask_workspace_bytes(n, m, N) bytes, 8-byte aligned, owned by
+ *           the caller; nothing in it needs initialising, and it must not be
+ *           reused until the work enqueued here has finished.
+ * stream:   hipStream_t (NULL = the null stream).  Enqueues four kernels and
+ *           returns without waiting.
+ * Errors:   NULL, DTYPE, ARG (sizes, N < 1, p outside [0, 1], misaligned
+ *           workspace), BUFSIZE (too small a workspace, layer beyond int32
+ *           indexing), HIP (launch failed).  On an error nothing is enqueued
+ *           (a HIP error may leave earlier kernels of the call enqueued).
+ *           Unlike the host function, NaN weights are not detected: their
+ *           norms order above every number, perm stays a permutation and the
+ *           mask keeps exactly t blocks.
+ */
+size_t onexn_mask_workspace_bytes(int32_t n, int32_t m, int32_t N);
+onexn_status onexn_build_mask_dev(const void* w_dev, onexn_dtype wdt, int32_t n, int32_t m,
+                                  int32_t kh, int32_t kw, int32_t N, double p, int32_t rearrange,
+                                  int32_t* perm_dev, uint8_t* mask_dev, int64_t* t,
+                                  void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /*
  * BSR packing (host, synchronous): Sec. 3.4 and Fig. 3.

@@ -26,7 +26,7 @@ _STATUS_NAMES = ["ONEXN_OK", "ONEXN_ERR_NULL", "ONEXN_ERR_ARG", "ONEXN_ERR_SHAPE
 F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 
-EXPORTED = ("onexn_build_mask", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
+EXPORTED = ("onexn_build_mask", "onexn_mask_workspace_bytes", "onexn_build_mask_dev", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
             "onexn_fc_fwd", "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
 ACTS = {"none": 0, "relu": 1, "relu6": 2}
 
@@ -53,6 +53,12 @@ def load_library():
     lib.onexn_build_mask.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32,
                                      ctypes.c_double, c_i32, c_vp, c_vp, c_vp]
     lib.onexn_build_mask.restype = ctypes.c_int
+    lib.onexn_mask_workspace_bytes.argtypes = [c_i32, c_i32, c_i32]
+    lib.onexn_mask_workspace_bytes.restype = ctypes.c_size_t
+    lib.onexn_build_mask_dev.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                         ctypes.c_double, c_i32, c_vp, c_vp, c_vp, c_vp,
+                                         ctypes.c_size_t, c_vp]
+    lib.onexn_build_mask_dev.restype = ctypes.c_int
     lib.onexn_pack.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp,
                                c_i64, c_vp, c_vp, c_vp]
     lib.onexn_pack.restype = ctypes.c_int
@@ -125,6 +131,39 @@ def build_mask(w: torch.Tensor, N: int, p: float, rearrange: bool) -> Tuple[torc
                                          float(p), int(bool(rearrange)), perm.data_ptr(),
                                          mask.data_ptr(), ctypes.addressof(t))
     _check(st, "onexn_build_mask")
+    return perm, mask, int(t.value)
+
+
+def mask_workspace_bytes(n: int, m: int, N: int) -> int:
+    """``onexn_mask_workspace_bytes``: device scratch that build_mask_dev needs."""
+    return int(load_library().onexn_mask_workspace_bytes(int(n), int(m), int(N)))
+
+
+def build_mask_dev(w: torch.Tensor, N: int, p: float, rearrange: bool,
+                   workspace: Optional[torch.Tensor] = None, stream: Optional[int] = None):
+    """``onexn_build_mask_dev`` on a device weight: returns (perm int32[n],
+    mask uint8[m][G], both on the device, and t).  Enqueued on ``stream``
+    (default: torch's current stream); ``workspace`` (a device uint8 tensor of
+    at least mask_workspace_bytes bytes) is allocated here when not given."""
+    if w.dim() != 4 or w.device.type != "cuda" or not w.is_contiguous():
+        raise ValueError("w must be a contiguous device tensor [n][m][kh][kw]")
+    n, m, kh, kw = w.shape
+    G = -(-n // int(N)) if N > 0 else 1
+    need = mask_workspace_bytes(n, m, N)
+    if workspace is None:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=w.device)
+    elif workspace.device.type != "cuda" or workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous device uint8 tensor")
+    perm = torch.empty(n, dtype=torch.int32, device=w.device)
+    mask = torch.empty((m, G), dtype=torch.uint8, device=w.device)
+    t = ctypes.c_int64(0)
+    if stream is None:
+        stream = torch.cuda.current_stream(w.device).cuda_stream
+    st = load_library().onexn_build_mask_dev(w.data_ptr(), _dtype_code(w.dtype), n, m, kh, kw, int(N),
+                                             float(p), int(bool(rearrange)), perm.data_ptr(),
+                                             mask.data_ptr(), ctypes.addressof(t), workspace.data_ptr(),
+                                             workspace.numel(), stream)
+    _check(st, "onexn_build_mask_dev")
     return perm, mask, int(t.value)
 
 
@@ -309,6 +348,7 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
     return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
 
 
-__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "fc_fwd", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
+__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "build_mask_dev", "fc_fwd",
+           "mask_workspace_bytes", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
            "prepare_layer", "set_tuning", "status_string"]

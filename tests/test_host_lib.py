@@ -262,3 +262,27 @@ def test_fused_conv_rejects_unknown_activation_before_any_launch(lib):
                                     None, 0, None, None, 2, None)
     assert st == 0   # batch 0 with a valid activation: a no-op
 
+
+
+def test_build_mask_dev_checks_arguments_on_the_host(lib):
+    """onexn_build_mask_dev validates before enqueuing anything, so its errors
+    show without a GPU; the workspace size grows with n and m * G."""
+    assert lib.onexn_mask_workspace_bytes(32, 16, 8) >= 8 * (32 + 16 * 4)
+    assert lib.onexn_mask_workspace_bytes(0, 16, 8) == 0
+    dummy = ctypes.c_int64(0)
+    p = ctypes.addressof(dummy)
+    t = ctypes.c_int64(-1)
+    base = [p, 0, 32, 16, 3, 3, 8, 0.5, 1, p, p, ctypes.addressof(t)]
+
+    def call(i, v, ws=p, wsb=1 << 20):
+        args = list(base)
+        args[i] = v
+        return lib.onexn_build_mask_dev(*args, ws, wsb, None)
+    assert call(0, None) == ERR["ONEXN_ERR_NULL"]
+    assert call(1, 7) == ERR["ONEXN_ERR_DTYPE"]
+    assert call(2, 0) == ERR["ONEXN_ERR_ARG"]
+    assert call(6, 0) == ERR["ONEXN_ERR_ARG"]
+    assert call(7, 1.5) == ERR["ONEXN_ERR_ARG"]
+    assert call(7, 0.5, None) == ERR["ONEXN_ERR_NULL"]
+    assert call(7, 0.5, p, 8) == ERR["ONEXN_ERR_BUFSIZE"]
+    assert t.value == -1
