@@ -108,6 +108,23 @@ onexn_status onexn_build_mask_dev(const void* w_dev, onexn_dtype wdt, int32_t n,
                                   void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /*
+ * onexn_build_mask_dev without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments (minus the workspace),
+ * results and errors as onexn_build_mask_dev; it allocates nothing.  The
+ * workspace is a fixed 8 MiB array in the library that each GPU holds from
+ * the library's load until the process ends: layers needing more
+ * (onexn_mask_workspace_bytes(n, m, N) > 8 MiB) fail with
+ * ONEXN_ERR_BUFSIZE.  Every call on a GPU shares that GPU's array: calls
+ * whose work overlaps on one GPU (on different streams, or from several
+ * threads without ordering) race on it and give undefined results.
+ */
+onexn_status onexn_build_mask_dev_noalloc(const void* w_dev, onexn_dtype wdt, int32_t n, int32_t m,
+                                          int32_t kh, int32_t kw, int32_t N, double p,
+                                          int32_t rearrange, int32_t* perm_dev, uint8_t* mask_dev,
+                                          int64_t* t, void* stream);
+
+/*
  * BSR packing (host, synchronous): Sec. 3.4 and Fig. 3.
  *
  * Encodes Omega-bar = rearranged W masked by `mask` (Eq. 6) into

@@ -26,7 +26,8 @@ _STATUS_NAMES = ["ONEXN_OK", "ONEXN_ERR_NULL", "ONEXN_ERR_ARG", "ONEXN_ERR_SHAPE
 F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 
-EXPORTED = ("onexn_build_mask", "onexn_mask_workspace_bytes", "onexn_build_mask_dev", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
+EXPORTED = ("onexn_build_mask", "onexn_mask_workspace_bytes", "onexn_build_mask_dev",
+            "onexn_build_mask_dev_noalloc", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
             "onexn_fc_fwd", "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
 ACTS = {"none": 0, "relu": 1, "relu6": 2}
 
@@ -59,6 +60,9 @@ def load_library():
                                          ctypes.c_double, c_i32, c_vp, c_vp, c_vp, c_vp,
                                          ctypes.c_size_t, c_vp]
     lib.onexn_build_mask_dev.restype = ctypes.c_int
+    lib.onexn_build_mask_dev_noalloc.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                                 ctypes.c_double, c_i32, c_vp, c_vp, c_vp, c_vp]
+    lib.onexn_build_mask_dev_noalloc.restype = ctypes.c_int
     lib.onexn_pack.argtypes = [c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp,
                                c_i64, c_vp, c_vp, c_vp]
     lib.onexn_pack.restype = ctypes.c_int

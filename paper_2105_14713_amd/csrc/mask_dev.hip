@@ -39,11 +39,46 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "onexn_internal.h"
 
+// Scratch of the no-allocation entry point (onexn_build_mask_dev_noalloc):
+// the workspace of one mask build, 8 MiB, so layers with n + m * G up to about
+// a million fit (the 2048 -> 2048 layer at N = 32 needs 1.1 MB).  Every GPU the
+// library runs on holds its own copy from the program's load until the
+// process ends.  In host code this name stands for the array but is not a
+// device address: host code uses the address hipGetSymbolAddress returns.
+static __device__ __align__(256) unsigned char scratch[size_t(8) << 20];
+
 namespace onexn {
 namespace {
+
+constexpr size_t kScratchBytes = size_t(8) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, looked up once per
+// device (with that device current) and kept.
+onexn_status scratch_address(void** out) {
+    int dev = 0;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(ONEXN_ERR_HIP, "build_mask_dev_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(ONEXN_ERR_UNSUPPORTED, "build_mask_dev_noalloc: device %d beyond %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        const hipError_t se = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (se != hipSuccess || !p)
+            return fail(ONEXN_ERR_HIP, "build_mask_dev_noalloc: hipGetSymbolAddress(scratch): %s",
+                        hipGetErrorString(se));
+        g_scratch_addr[dev] = p;
+    }
+    *out = g_scratch_addr[dev];
+    return ONEXN_OK;
+}
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelBins = 256;
@@ -290,4 +325,22 @@ extern "C" onexn_status onexn_build_mask_dev(const void* w_dev, onexn_dtype wdt,
         return fail(ONEXN_ERR_ARG, "build_mask_dev: workspace must be 8-byte aligned");
     return build_mask_dev(w_dev, wdt, n, m, kh, kw, N, p, rearrange, perm_dev, mask_dev, t,
                           workspace_dev, workspace_bytes_, stream);
+}
+
+extern "C" onexn_status onexn_build_mask_dev_noalloc(const void* w_dev, onexn_dtype wdt, int32_t n,
+                                                     int32_t m, int32_t kh, int32_t kw, int32_t N,
+                                                     double p, int32_t rearrange, int32_t* perm_dev,
+                                                     uint8_t* mask_dev, int64_t* t, void* stream) {
+    clear_error();
+    if (onexn_status st = check_mask_args(w_dev, wdt, n, m, kh, kw, N, p, perm_dev, mask_dev, t)) return st;
+    const int64_t G = (int64_t(n) + N - 1) / N;
+    const size_t need = workspace_bytes(n, int64_t(m) * G);
+    if (need > kScratchBytes)
+        return fail(ONEXN_ERR_BUFSIZE,
+                    "build_mask_dev_noalloc: the layer needs %zu bytes of scratch, the entry point holds "
+                    "%zu (use onexn_build_mask_dev with a workspace)", need, kScratchBytes);
+    void* ws = nullptr;
+    if (onexn_status st = scratch_address(&ws)) return st;
+    return build_mask_dev(w_dev, wdt, n, m, kh, kw, N, p, rearrange, perm_dev, mask_dev, t, ws,
+                          kScratchBytes, stream);
 }
