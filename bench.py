@@ -213,6 +213,55 @@ def cpu_baseline(layers, batch, wl, budget_s, single_budget_s):
             "paper_context": PAPER_CPU_CONTEXT}
 
 
+def mask_bench(wl, dev, reps):
+    """Times onexn_build_mask_dev (GPU mask building: filter norms, ranks, block
+    scores, top-(1-p) selection) on every layer of a workload against the host
+    library's onexn_build_mask, after checking that both agree bit for bit."""
+    stream = torch.cuda.current_stream(dev)
+    rows, t_gpu, t_host, b_alg = [], 0.0, 0.0, 0.0
+    for layer in wl.layers:
+        w, _ = workloads.gen_layer(layer, 1, wl.dtype)
+        wd = w.to(dev)
+        ws = torch.empty(max(onexn.mask_workspace_bytes(*w.shape[:2], layer.N), 8), dtype=torch.uint8,
+                         device=dev)
+        h0 = time.perf_counter()
+        perm_h, mask_h, t_h = onexn.build_mask(w, layer.N, layer.p, layer.rearrange)
+        th = time.perf_counter() - h0
+        perm_d, mask_d, t_d = onexn.build_mask_dev(wd, layer.N, layer.p, layer.rearrange, ws)
+        torch.cuda.synchronize()
+        if not (t_d == t_h and torch.equal(perm_d.cpu(), perm_h) and torch.equal(mask_d.cpu(), mask_h)):
+            print(json.dumps({"parity": "FAIL", "layer": layer.name}), flush=True)
+            sys.exit(3)
+        for _ in range(3):
+            onexn.build_mask_dev(wd, layer.N, layer.p, layer.rearrange, ws)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            onexn.build_mask_dev(wd, layer.N, layer.p, layer.rearrange, ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tg = e0.elapsed_time(e1) / reps / 1e3
+        # Algorithmic bytes: W once for the block scores (once more for the
+        # filter norms), the scores written and read by the selection, the mask.
+        K = layer.cin * -(-layer.cout // layer.N)
+        wb = w.numel() * w.element_size()
+        bb = wb * (2 if layer.rearrange else 1) + 16 * K + K + 4 * layer.cout
+        rows.append({"layer": layer.name, "n": layer.cout, "m": layer.cin, "k": layer.k, "N": layer.N,
+                     "blocks": K, "gpu_us": round(tg * 1e6, 2), "host_us": round(th * 1e6, 1),
+                     "mb_alg": round(bb / 1e6, 3)})
+        t_gpu, t_host, b_alg = t_gpu + tg, t_host + th, b_alg + bb
+    t_roof = b_alg / (PEAK_HBM_GBPS * 1e9)
+    print(json.dumps({
+        "metric": "1xN mask building on the GPU (rearrangement, block l1 scores, top-(1-p)): "
+                  "time per workload, bit-exact with the host",
+        "value": round(t_gpu * 1e6, 2), "unit": "us", "higher_is_better": False, "n_gpus": 1,
+        "config": {"workload": wl.name, "layers": len(wl.layers)},
+        "host_us": round(t_host * 1e6, 1), "speedup_vs_host": round(t_host / t_gpu, 2),
+        "roofline": {"bound": "hbm", "achieved": round(b_alg / t_gpu / 1e9, 1), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(t_roof / t_gpu, 4), "traffic": None},
+        "per_layer": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -223,6 +272,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--cpu-single-budget", type=float, default=8.0,
                     help="seconds of single-threaded oracle work")
+    ap.add_argument("--mask", action="store_true",
+                    help="time the GPU mask building of the workload's layers instead of the conv")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a copy kernel of known size (for scaling byte counters)")
     args = ap.parse_args()
@@ -240,6 +291,9 @@ def main():
         copy_calibration(dev)
         return
     wl = WORKLOADS[args.workload]()
+    if args.mask:
+        mask_bench(wl, dev, max(args.steps, 5))
+        return
     batch = wl.batch
     odt = _TDT[wl.out_dtype]
     stream = torch.cuda.current_stream(dev)

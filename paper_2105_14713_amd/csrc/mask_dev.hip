@@ -185,25 +185,51 @@ __global__ void __launch_bounds__(kSelThreads) mask_select(const double* __restr
         sPrefix = 0;
         sNeed = kept;
     }
+    const int lane = tid & 63;
     uint64_t pmask = 0;
     for (int shift = 56; shift >= 0; shift -= 8) {
         for (int b = tid; b < kSelBins; b += kSelThreads) hist[b] = 0;
         __syncthreads();
         const uint64_t prefix = sPrefix;
-        for (int64_t i = tid; i < K; i += kSelThreads) {
-            const uint64_t key = order_key(score[i]);
-            if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 0xff], 1u);
+        const int64_t need = sNeed;
+        // Histogram of the next 8 bits of the candidates.  In the first
+        // passes most keys share their top bits: when every candidate lane of
+        // a wave hits one bin, a single atomic adds their count (same-address
+        // atomics of a whole wave would otherwise serialise).
+        for (int64_t i0 = 0; i0 < K; i0 += kSelThreads) {
+            const int64_t i = i0 + tid;
+            uint64_t key = 0;
+            if (i < K) key = order_key(score[i]);
+            const bool cand = i < K && (key & pmask) == prefix;
+            const uint32_t bin = uint32_t(key >> shift) & 0xff;
+            const uint64_t active = __ballot(cand);
+            if (active) {
+                const int leader = __ffsll(static_cast<unsigned long long>(active)) - 1;
+                const uint32_t lb = __shfl(bin, leader);
+                if (__ballot(cand && bin == lb) == active) {
+                    if (lane == leader) atomicAdd(&hist[lb], uint32_t(__popcll(active)));
+                } else if (cand) {
+                    atomicAdd(&hist[bin], 1u);
+                }
+            }
         }
         __syncthreads();
-        if (tid == 0) {
-            int64_t need = sNeed, above = 0;
-            int b = kSelBins - 1;
-            for (; b > 0; --b) {
-                if (above + int64_t(hist[b]) >= need) break;
-                above += hist[b];
+        // Counts from the top bin down (thread c holds bins 255 - c and
+        // above): the bin where they reach `need` holds the need-th key.
+        if (tid < kSelBins) scan[tid] = hist[kSelBins - 1 - tid];
+        __syncthreads();
+        for (int d = 1; d < kSelBins; d <<= 1) {
+            const int64_t v = (tid < kSelBins && tid >= d) ? scan[tid - d] : 0;
+            __syncthreads();
+            if (tid < kSelBins) scan[tid] += v;
+            __syncthreads();
+        }
+        if (tid < kSelBins) {
+            const int64_t upto = scan[tid], before = tid > 0 ? scan[tid - 1] : 0;
+            if (upto >= need && before < need) {
+                sNeed = need - before;
+                sPrefix = prefix | (uint64_t(kSelBins - 1 - tid) << shift);
             }
-            sNeed = need - above;
-            sPrefix = prefix | (uint64_t(b) << shift);
         }
         pmask |= uint64_t(0xff) << shift;
         __syncthreads();
