@@ -14,6 +14,10 @@ Everything is computed in fp64 by the plain C in ``oracle.c`` (Lin et al.,
 * ``pack``             - Sec. 3.4, Fig. 3: BSR arrays (P, I, D).
 * ``conv2d`` / ``conv2d_at`` - Eq. 7: direct convolution with Omega-bar.
 * ``decode``           - Eq. 8: block-wise decode over (P, I, D).
+* ``conv2d_bwd_data`` / ``conv2d_bwd_weight`` - the backward of Eq. 7 for
+                         fine-tuning with the pattern fixed (Sec. 4.1): the
+                         adjoint through Omega-bar, and the weight gradient on
+                         the kept blocks only.
 * ``epilogue``         - per-channel scale/bias and ReLU/ReLU6 after a conv
                          (folded batch norm of the Sec. 4.1 networks).
 * ``prune``            - the offline steps chained: perm, T, t, Omega-bar, BSR.
@@ -21,12 +25,14 @@ Everything is computed in fp64 by the plain C in ``oracle.c`` (Lin et al.,
 Every function takes and returns numpy arrays; weights and activations are
 float64 (fp32 and bf16 values widen exactly).
 """
-from .oracle import (apply_perm, block_scores, conv2d, conv2d_at, decode, epilogue, filter_norms,
+from .oracle import (apply_perm, block_scores, conv2d, conv2d_at, conv2d_bwd_data, conv2d_bwd_weight,
+                     decode, epilogue, filter_norms,
                      filter_perm,
                      kept_count, masked_weight, num_threads, pack, prune, select,
                      set_num_threads)
 
-__all__ = ["apply_perm", "block_scores", "conv2d", "conv2d_at", "decode", "epilogue", "filter_norms",
+__all__ = ["apply_perm", "block_scores", "conv2d", "conv2d_at", "conv2d_bwd_data", "conv2d_bwd_weight",
+           "decode", "epilogue", "filter_norms",
            "filter_perm",
            "kept_count", "masked_weight", "num_threads", "pack", "prune", "select",
            "set_num_threads"]

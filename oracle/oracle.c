@@ -332,6 +332,75 @@ void oracle_epilogue(double* y, int B, int n, int64_t hw, const double* scale, c
 }
 
 /* ---------------------------------------------------------------------- */
+/* Backward of Eq. 7 for fine-tuning with the 1xN pattern fixed (Sec. 4.1). */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * Gradient with respect to the input: the adjoint of Eq. 7.  Every term
+ * X[b][c][ih][iw] * Wbar[o][c][q][r] of output (b, o, oh, ow) sends
+ * dY[b][o][oh][ow] * Wbar[o][c][q][r] back to X[b][c][ih][iw].
+ * dy[B][n][Ho][Wo] in, dx[B][m][H][W] out.
+ */
+void oracle_conv2d_bwd_data(const double* dy, const double* wbar, int B, int m, int H, int W, int n,
+                            int h, int wd, int sh, int sw, int ph, int pw, double* dx)
+{
+    int Ho = (H + 2 * ph - h) / sh + 1;
+    int Wo = (W + 2 * pw - wd) / sw + 1;
+    memset(dx, 0, sizeof(double) * (size_t)B * m * H * W);
+#pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; b++)
+        for (int o = 0; o < n; o++)
+            for (int oh = 0; oh < Ho; oh++)
+                for (int ow = 0; ow < Wo; ow++) {
+                    double g = dy[(((int64_t)b * n + o) * Ho + oh) * Wo + ow];
+                    for (int c = 0; c < m; c++)
+                        for (int q = 0; q < h; q++)
+                            for (int r = 0; r < wd; r++) {
+                                int ih = oh * sh - ph + q;
+                                int iw = ow * sw - pw + r;
+                                if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
+                                dx[(((int64_t)b * m + c) * H + ih) * W + iw] +=
+                                    g * wbar[(((int64_t)o * m + c) * h + q) * wd + r];
+                            }
+                }
+}
+
+/*
+ * Gradient with respect to the weights, restricted to the kept 1xN blocks:
+ * the weights of pruned blocks stay zero during fine-tuning, so their
+ * gradient is not used and is returned as 0.
+ *   dw[o][c][q][r] = T[c][o/N] * sum_{b,oh,ow} dY[b][o][oh][ow] * X[b][c][oh*sh-ph+q][ow*sw-pw+r]
+ * x[B][m][H][W], dy[B][n][Ho][Wo], T[m][G] in; dw[n][m][h][w] out.
+ */
+void oracle_conv2d_bwd_weight(const double* x, const double* dy, const uint8_t* T, int B, int m, int H,
+                              int W, int n, int h, int wd, int N, int sh, int sw, int ph, int pw,
+                              double* dw)
+{
+    int Ho = (H + 2 * ph - h) / sh + 1;
+    int Wo = (W + 2 * pw - wd) / sw + 1;
+    int G = (n + N - 1) / N;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int o = 0; o < n; o++)
+        for (int c = 0; c < m; c++)
+            for (int q = 0; q < h; q++)
+                for (int r = 0; r < wd; r++) {
+                    double acc = 0.0;
+                    if (T[(int64_t)c * G + o / N]) {
+                        for (int b = 0; b < B; b++)
+                            for (int oh = 0; oh < Ho; oh++)
+                                for (int ow = 0; ow < Wo; ow++) {
+                                    int ih = oh * sh - ph + q;
+                                    int iw = ow * sw - pw + r;
+                                    if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
+                                    acc += dy[(((int64_t)b * n + o) * Ho + oh) * Wo + ow] *
+                                           x[(((int64_t)b * m + c) * H + ih) * W + iw];
+                                }
+                    }
+                    dw[(((int64_t)o * m + c) * h + q) * wd + r] = acc;
+                }
+}
+
+/* ---------------------------------------------------------------------- */
 /* Eq. 8: block-wise decode over the BSR arrays.                           */
 /* ---------------------------------------------------------------------- */
 

@@ -45,6 +45,8 @@ def _load():
     lib.oracle_conv2d_at.argtypes = [_f64p, _f64p] + [_int] * 11 + [_i64p, ctypes.c_int64, _f64p]
     lib.oracle_epilogue.argtypes = [_f64p, _int, _int, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p, _int]
+    lib.oracle_conv2d_bwd_data.argtypes = [_f64p, _f64p] + [_int] * 11 + [_f64p]
+    lib.oracle_conv2d_bwd_weight.argtypes = [_f64p, _f64p, _u8p] + [_int] * 12 + [_f64p]
     lib.oracle_decode.argtypes = [_f64p, _i32p, _i32p, _f64p] + [_int] * 12 + [_f64p]
     _lib = lib
     return lib
@@ -155,6 +157,35 @@ def conv2d_at(x, wbar, idx, stride=(1, 1), pad=(0, 0)):
     _load().oracle_conv2d_at(x, wbar, B, m, H, W, n, h, wd, stride[0], stride[1], pad[0], pad[1],
                              idx, idx.size, out)
     return out
+
+
+def conv2d_bwd_data(dy, wbar, input_hw, stride=(1, 1), pad=(0, 0)):
+    """dL/dX of Eq. 7: dy[B][n][Ho][Wo], wbar[n][m][h][w] -> dx[B][m][H][W] (fp64)."""
+    dy, wbar = _f64(dy), _f64(wbar)
+    B, n = dy.shape[0], dy.shape[1]
+    _, m, h, wd = wbar.shape
+    H, W = input_hw
+    assert (dy.shape[2], dy.shape[3]) == _out_hw(H, W, h, wd, stride, pad)
+    dx = np.empty((B, m, H, W), np.float64)
+    _load().oracle_conv2d_bwd_data(dy, wbar, B, m, H, W, n, h, wd, stride[0], stride[1], pad[0],
+                                   pad[1], dx)
+    return dx
+
+
+def conv2d_bwd_weight(x, dy, T, N, kernel_hw, stride=(1, 1), pad=(0, 0)):
+    """dL/dW of Eq. 7 on the kept 1xN blocks of mask T[m][G] (0 elsewhere):
+    x[B][m][H][W], dy[B][n][Ho][Wo] -> dw[n][m][h][w] (fp64, rearranged rows)."""
+    x, dy = _f64(x), _f64(dy)
+    B, m, H, W = x.shape
+    n = dy.shape[1]
+    h, wd = kernel_hw
+    assert (dy.shape[2], dy.shape[3]) == _out_hw(H, W, h, wd, stride, pad)
+    T = np.ascontiguousarray(T, np.uint8)
+    assert T.shape == (m, -(-n // N))
+    dw = np.empty((n, m, h, wd), np.float64)
+    _load().oracle_conv2d_bwd_weight(x, dy, T, B, m, H, W, n, h, wd, int(N), stride[0], stride[1],
+                                     pad[0], pad[1], dw)
+    return dw
 
 
 _ACTS = {"none": 0, "relu": 1, "relu6": 2}

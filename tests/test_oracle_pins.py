@@ -369,3 +369,68 @@ def test_pack_invariants(oracle_lib, n, m, k, N, p):
     np.testing.assert_array_equal(dense_from_bsr(pr.P, pr.I, pr.D, n, m), pr.wbar)
     if n % N:
         assert not np.any(pr.D[pr.P[G - 1]:, n % N:])
+
+
+# ---------------------------------------------------------------------------
+# Backward of Eq. 7 (fine-tuning with the 1xN pattern fixed).
+# ---------------------------------------------------------------------------
+
+BWD_SHAPES = [  # (n, m, k, stride, pad, B, H, W, N)
+    (12, 5, 1, 1, 0, 2, 6, 5, 4),
+    (10, 7, 3, 1, 1, 2, 7, 6, 4),      # ragged last col-group
+    (16, 3, 3, 2, 1, 1, 9, 8, 8),
+    (8, 3, 7, 2, 3, 1, 11, 10, 4),
+    (9, 6, 1, 2, 0, 2, 7, 7, 2),
+]
+
+
+@pytest.mark.parametrize("shape", BWD_SHAPES, ids=lambda s: "n%d_m%d_k%d_s%d_p%d" % s[:5])
+def test_bwd_equals_torch_conv_gradients(oracle_lib, shape):
+    """dX equals torch's conv2d_input with the masked weight; dW equals torch's
+    conv2d_weight times the 1xN mask (fp64 library routines)."""
+    n, m, k, s, pd, B, H, W, N = shape
+    rng = np.random.default_rng(n * m + k)
+    w = rng.standard_normal((n, m, k, k))
+    x = rng.standard_normal((B, m, H, W))
+    pr = oracle_lib.prune(w, N, 0.5, True)
+    Ho, Wo = (H + 2 * pd - k) // s + 1, (W + 2 * pd - k) // s + 1
+    dy = rng.standard_normal((B, n, Ho, Wo))
+    dx = oracle_lib.conv2d_bwd_data(dy, pr.wbar, (H, W), (s, s), (pd, pd))
+    ref_dx = torch.nn.grad.conv2d_input((B, m, H, W), torch.from_numpy(pr.wbar), torch.from_numpy(dy),
+                                        stride=s, padding=pd)
+    np.testing.assert_allclose(dx, ref_dx.numpy(), rtol=1e-12, atol=1e-12)
+    dw = oracle_lib.conv2d_bwd_weight(x, dy, pr.T, N, (k, k), (s, s), (pd, pd))
+    ref_dw = torch.nn.grad.conv2d_weight(torch.from_numpy(x), (n, m, k, k), torch.from_numpy(dy),
+                                         stride=s, padding=pd).numpy()
+    keep = np.repeat(pr.T.T, N, axis=0)[:n][:, :, None, None]     # [n][m] kept-block mask
+    np.testing.assert_allclose(dw, ref_dw * keep, rtol=1e-12, atol=1e-12)
+    assert np.all(dw[keep[:, :, 0, 0] == 0] == 0)
+
+
+@pytest.mark.parametrize("shape", BWD_SHAPES, ids=lambda s: "n%d_m%d_k%d_s%d_p%d" % s[:5])
+def test_bwd_adjoint_identities(oracle_lib, shape):
+    """Eq. 7 is bilinear in (X, Wbar), so with integer data, exactly:
+    <conv(X, Wbar), dY> = <X, dX>  and  <conv(X, V), dY> = <dW, V> for any V
+    with the same 1xN mask (no library routine involved)."""
+    n, m, k, s, pd, B, H, W, N = shape
+    rng = np.random.default_rng(7 * n + m)
+    w = rng.integers(-3, 4, (n, m, k, k)).astype(np.float64)
+    x = rng.integers(-2, 3, (B, m, H, W)).astype(np.float64)
+    pr = oracle_lib.prune(w, N, 0.5, True)
+    y = oracle_lib.conv2d(x, pr.wbar, (s, s), (pd, pd))
+    dy = rng.integers(-2, 3, y.shape).astype(np.float64)
+    dx = oracle_lib.conv2d_bwd_data(dy, pr.wbar, (H, W), (s, s), (pd, pd))
+    assert np.sum(y * dy) == np.sum(x * dx)
+    v = oracle_lib.masked_weight(rng.integers(-3, 4, (n, m, k, k)).astype(np.float64), pr.T, N)
+    dw = oracle_lib.conv2d_bwd_weight(x, dy, pr.T, N, (k, k), (s, s), (pd, pd))
+    assert np.sum(oracle_lib.conv2d(x, v, (s, s), (pd, pd)) * dy) == np.sum(dw * v)
+
+
+def test_bwd_with_everything_pruned_is_zero(oracle_lib):
+    rng = np.random.default_rng(3)
+    w = rng.standard_normal((8, 4, 3, 3))
+    x = rng.standard_normal((1, 4, 5, 5))
+    pr = oracle_lib.prune(w, 4, 1.0, False)
+    dy = rng.standard_normal((1, 8, 5, 5))
+    assert np.all(oracle_lib.conv2d_bwd_data(dy, pr.wbar, (5, 5), (1, 1), (1, 1)) == 0)
+    assert np.all(oracle_lib.conv2d_bwd_weight(x, dy, pr.T, 4, (3, 3), (1, 1), (1, 1)) == 0)
