@@ -210,6 +210,37 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
                                     void* stream);
 
 /*
+ * Backward of the 1xN-pruned convolution (device, asynchronous), for
+ * fine-tuning with the pattern fixed (Sec. 4.1): the pruned weights stay
+ * zero, so only the kept blocks' weights get a gradient.  NCHW only.
+ *
+ * onexn_conv2d_bwd_data: the input gradient, the adjoint of Eq. 7 through
+ *   Omega-bar:  dX[b][c][ih][iw] = sum over kept blocks z with I[z] = c, rows i
+ *   and taps (q, r) landing on (ih, iw) of D[z][i][q][r] * dY[b][gN+i][oh][ow].
+ *   dy_dev [batch][n][Ho][Wo] (rearranged channel order, as the forward's y)
+ *   in dydt == wdt; dx_dev [batch][m][H][W] in dxdt (dydt or F32).  Every dx
+ *   element is written.  Layers with more than 2048 col-groups: UNSUPPORTED.
+ * onexn_conv2d_bwd_weight: the gradient of the kept blocks in D's layout,
+ *   dD[z][i][q][r] = sum_{b,oh,ow} dY[b][gN+i][oh][ow] * X[b][I[z]][oh*sh-ph+q][ow*sw-pw+r],
+ *   fp32 [t][N][kh][kw] (rows gN+i >= n get 0); x_dev [batch][m][H][W] and
+ *   dy_dev in xdt (F32 or BF16).
+ * Both accumulate in fp32 in a fixed order (results do not vary run to run).
+ * Arguments, ownership, the int32 size limits and the errors are those of
+ * onexn_conv2d_fwd; P, I, D are the forward's BSR arrays.
+ */
+onexn_status onexn_conv2d_bwd_data(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
+                                   onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw,
+                                   int32_t N, int64_t t, const void* dy_dev, onexn_dtype dydt,
+                                   int32_t batch, int32_t H, int32_t W, int32_t stride_h,
+                                   int32_t stride_w, int32_t pad_h, int32_t pad_w, void* dx_dev,
+                                   onexn_dtype dxdt, void* stream);
+onexn_status onexn_conv2d_bwd_weight(const int32_t* P_dev, const int32_t* I_dev, int32_t n, int32_t m,
+                                     int32_t kh, int32_t kw, int32_t N, int64_t t, const void* x_dev,
+                                     onexn_dtype xdt, const void* dy_dev, int32_t batch, int32_t H,
+                                     int32_t W, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                     int32_t pad_w, float* dD_dev, void* stream);
+
+/*
  * Fully connected layer (device, asynchronous): Sec. 3.1 treats an FC layer
  * as the kh = kw = 1 case, so its weight [n][m] is packed like a 1x1 conv
  * (onexn_build_mask / onexn_pack with kh = kw = 1) and

@@ -28,7 +28,7 @@ NCHW, NHWC = 0, 1
 
 EXPORTED = ("onexn_build_mask", "onexn_mask_workspace_bytes", "onexn_build_mask_dev",
             "onexn_build_mask_dev_noalloc", "onexn_pack", "onexn_conv2d_fwd", "onexn_conv2d_fwd_fused",
-            "onexn_fc_fwd", "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
+            "onexn_conv2d_bwd_data", "onexn_conv2d_bwd_weight", "onexn_fc_fwd", "onexn_set_tuning", "onexn_status_string", "onexn_last_error")
 ACTS = {"none": 0, "relu": 1, "relu6": 2}
 
 _lib = None
@@ -74,6 +74,12 @@ def load_library():
                                            [c_vp, ctypes.c_int, ctypes.c_int] + [c_i32] * 7 +
                                            [c_vp, ctypes.c_int, c_vp, c_vp, ctypes.c_int, c_vp])
     lib.onexn_conv2d_fwd_fused.restype = ctypes.c_int
+    lib.onexn_conv2d_bwd_data.argtypes = ([c_vp, c_vp, c_vp, ctypes.c_int] + [c_i32] * 5 + [c_i64] +
+                                          [c_vp, ctypes.c_int] + [c_i32] * 7 + [c_vp, ctypes.c_int, c_vp])
+    lib.onexn_conv2d_bwd_data.restype = ctypes.c_int
+    lib.onexn_conv2d_bwd_weight.argtypes = ([c_vp, c_vp] + [c_i32] * 5 + [c_i64] + [c_vp, ctypes.c_int, c_vp] +
+                                            [c_i32] * 7 + [c_vp, c_vp])
+    lib.onexn_conv2d_bwd_weight.restype = ctypes.c_int
     lib.onexn_fc_fwd.argtypes = ([c_vp, c_vp, c_vp, ctypes.c_int, c_i32, c_i32, c_i32, c_i64, c_vp,
                                   ctypes.c_int, ctypes.c_int, c_i32, c_vp, ctypes.c_int, c_vp, c_vp,
                                   ctypes.c_int, c_vp])
@@ -264,6 +270,65 @@ def conv2d_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: tor
     return out
 
 
+def _dev_contig(**tensors):
+    for name, tns in tensors.items():
+        if tns.device.type != "cuda" or not tns.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+
+
+def conv2d_bwd_data(P, I, D, n: int, m: int, dy: torch.Tensor, input_hw, stride=1, pad=0,
+                    out_dtype: Optional[torch.dtype] = None, out: Optional[torch.Tensor] = None,
+                    stream: Optional[int] = None) -> torch.Tensor:
+    """``onexn_conv2d_bwd_data``: dX [B][m][H][W] of the 1xN conv from dY
+    [B][n][Ho][Wo] (NCHW, rearranged output channels)."""
+    _dev_contig(P=P, I=I, D=D, dy=dy)
+    t, N, kh, kw = D.shape
+    B = dy.shape[0]
+    H, W = input_hw
+    stride, pad = _pair(stride), _pair(pad)
+    if tuple(dy.shape) != (B, n) + out_hw(H, W, kh, kw, stride, pad):
+        raise ValueError("dy does not have the layer's output shape")
+    odt = dy.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((B, m, H, W), dtype=odt, device=dy.device)
+    elif tuple(out.shape) != (B, m, H, W) or out.dtype != odt or not out.is_contiguous():
+        raise ValueError("out has the wrong shape, dtype or layout")
+    if stream is None:
+        stream = torch.cuda.current_stream(dy.device).cuda_stream
+    st = load_library().onexn_conv2d_bwd_data(
+        P.data_ptr(), I.data_ptr() if t else 0, D.data_ptr() if t else 0, _dtype_code(D.dtype), int(n),
+        int(m), kh, kw, N, t, dy.data_ptr(), _dtype_code(dy.dtype), B, H, W, stride[0], stride[1],
+        pad[0], pad[1], out.data_ptr(), _dtype_code(odt), stream)
+    _check(st, "onexn_conv2d_bwd_data")
+    return out
+
+
+def conv2d_bwd_weight(P, I, n: int, N: int, kernel_hw, x: torch.Tensor, dy: torch.Tensor, stride=1,
+                      pad=0, out: Optional[torch.Tensor] = None,
+                      stream: Optional[int] = None) -> torch.Tensor:
+    """``onexn_conv2d_bwd_weight``: the fp32 gradient dD [t][N][kh][kw] of the
+    kept blocks from X [B][m][H][W] and dY [B][n][Ho][Wo] (NCHW)."""
+    _dev_contig(P=P, I=I, x=x, dy=dy)
+    t = I.numel()
+    kh, kw = kernel_hw
+    B, m, H, W = x.shape
+    stride, pad = _pair(stride), _pair(pad)
+    if tuple(dy.shape) != (B, n) + out_hw(H, W, kh, kw, stride, pad) or dy.dtype != x.dtype:
+        raise ValueError("dy does not have the layer's output shape or x's dtype")
+    if out is None:
+        out = torch.empty((t, N, kh, kw), dtype=torch.float32, device=x.device)
+    elif tuple(out.shape) != (t, N, kh, kw) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous fp32 tensor [t][N][kh][kw]")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device).cuda_stream
+    st = load_library().onexn_conv2d_bwd_weight(
+        P.data_ptr(), I.data_ptr() if t else 0, int(n), m, kh, kw, int(N), t, x.data_ptr(),
+        _dtype_code(x.dtype), dy.data_ptr(), B, H, W, stride[0], stride[1], pad[0], pad[1],
+        out.data_ptr() if t else 0, stream)
+    _check(st, "onexn_conv2d_bwd_weight")
+    return out
+
+
 def fc_fwd(P: torch.Tensor, I: torch.Tensor, D: torch.Tensor, n: int, x: torch.Tensor,
            layout: str = "rows", out_dtype: Optional[torch.dtype] = None,
            out: Optional[torch.Tensor] = None, stream: Optional[int] = None,
@@ -352,7 +417,8 @@ def prepare_layer(w: torch.Tensor, N: int, p: float, rearrange: bool,
     return PackedLayer(n, m, kh, kw, int(N), t, perm, mask, P.to(dev), I.to(dev), D.to(dev))
 
 
-__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "build_mask_dev", "fc_fwd",
+__all__ = ["ACTS", "BF16", "BoundConv", "EXPORTED", "F32", "build_mask_dev", "conv2d_bwd_data",
+           "conv2d_bwd_weight", "fc_fwd",
            "mask_workspace_bytes", "LIB_PATH", "NCHW", "NHWC", "OnexnError", "PackedLayer",
            "build_mask", "conv2d_fwd", "last_error", "load_library", "out_hw", "pack",
            "prepare_layer", "set_tuning", "status_string"]

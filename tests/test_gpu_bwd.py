@@ -1,0 +1,115 @@
+"""GPU parity of the backward kernels (input gradient through Omega-bar, and
+the kept blocks' weight gradient in D's layout) against the oracle's
+backward of Eq. 7 on the same inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2105_14713_amd as onexn
+import workloads
+from gpu_helpers import rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    onexn.load_library()
+
+
+def _bwd(w, x, dy, N, p, s, pd, dx_dtype=None):
+    """(GPU dX, GPU dD, oracle dX, oracle dD) as fp64 numpy; w, x, dy on the host."""
+    n, m, k, _ = w.shape
+    H, W = x.shape[2], x.shape[3]
+    layer = onexn.prepare_layer(w, N, p, True)
+    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, n, m, dy.cuda(), (H, W), s, pd, dx_dtype)
+    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, n, N, (k, k), x.cuda(), dy.cuda(), s, pd)
+    torch.cuda.synchronize()
+    pr = oracle.prune(w.double().numpy(), N, p, True)
+    assert layer.t == pr.t
+    ref_dx = oracle.conv2d_bwd_data(dy.double().numpy(), pr.wbar, (H, W), (s, s), (pd, pd))
+    dw = oracle.conv2d_bwd_weight(x.double().numpy(), dy.double().numpy(), pr.T, N, (k, k), (s, s),
+                                  (pd, pd))
+    _, _, ref_dD = oracle.pack(dw, pr.T, N)
+    return dx.double().cpu().numpy(), dD.double().cpu().numpy(), ref_dx, ref_dD
+
+
+CASES = [  # (n, m, k, stride, pad, B, H, W, N)
+    (72, 13, 3, 1, 1, 2, 11, 9, 32),    # ragged last col-group
+    (40, 9, 3, 2, 1, 2, 12, 11, 16),
+    (18, 24, 1, 1, 0, 3, 7, 7, 4),
+    (28, 17, 1, 2, 0, 2, 9, 10, 8),
+    (9, 6, 7, 2, 3, 1, 15, 13, 2),
+    (7, 20, 5, 3, 2, 2, 13, 12, 1),
+    (64, 3, 7, 2, 3, 1, 20, 20, 32),    # stem-like
+]
+
+
+@pytest.mark.parametrize("p", [0.0, 0.5, 0.9])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "n%d_m%d_k%d_s%d_p%d_N%d" % (c[:5] + (c[8],)))
+def test_bwd_integer_exact(case, p):
+    n, m, k, s, pd, B, H, W, N = case
+    print(f"bwd {case} p={p}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=n + m + k, cout=n, cin=m, k=k, batch=B, H=H, W=W,
+                                       wmax=2, xmax=2)
+    Ho, Wo = (H + 2 * pd - k) // s + 1, (W + 2 * pd - k) // s + 1
+    gen = torch.Generator().manual_seed(n * k)
+    dy = torch.randint(-2, 3, (B, n, Ho, Wo), generator=gen).float()
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, p, s, pd)
+    np.testing.assert_array_equal(dx, ref_dx)
+    np.testing.assert_array_equal(dD, ref_dD)
+
+
+@pytest.mark.parametrize("case", CASES[:4], ids=lambda c: "n%d_m%d_k%d" % c[:3])
+def test_bwd_fp32_random(case):
+    n, m, k, s, pd, B, H, W, N = case
+    gen = torch.Generator().manual_seed(5 * n + m)
+    w = workloads.gen_weight(gen, n, m, k)
+    x = workloads.gen_activation(gen, (B, m, H, W))
+    Ho, Wo = (H + 2 * pd - k) // s + 1, (W + 2 * pd - k) // s + 1
+    dy = torch.randn((B, n, Ho, Wo), generator=gen)
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, 0.5, s, pd)
+    assert rel_err(dx, ref_dx) <= 1e-5
+    assert rel_err(dD, ref_dD) <= 1e-5
+
+
+@pytest.mark.parametrize("dx_dtype", [torch.float32, torch.bfloat16], ids=["dxf32", "dxbf16"])
+def test_bwd_bf16(dx_dtype):
+    """bf16 weights, activations and output gradient; fp32 accumulation.  The
+    oracle sees the same bf16 values; the bf16 dX has one final rounding."""
+    gen = torch.Generator().manual_seed(17)
+    w = workloads.gen_weight(gen, 64, 40, 3).bfloat16()
+    x = workloads.gen_activation(gen, (2, 40, 10, 10)).bfloat16()
+    dy = torch.randn((2, 64, 10, 10), generator=gen).bfloat16()
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, 32, 0.5, 1, 1, dx_dtype)
+    assert rel_err(dx, ref_dx) <= (2e-2 if dx_dtype == torch.bfloat16 else 1e-5)
+    assert rel_err(dD, ref_dD) <= 1e-5
+
+
+def test_bwd_resnet50_layer_shape_and_reproducibility():
+    """A ResNet-50 3x3 layer (256 -> 256 at 14x14, N = 32, p = 0.5) at batch 4:
+    fp32 random within 1e-5 of the oracle, and two runs bit-identical."""
+    layer = [l for l in workloads.resnet50_convs() if l.name == "s3b2_3x3"][0]
+    w, x = workloads.gen_layer(layer, 4)
+    gen = torch.Generator().manual_seed(99)
+    dy = torch.randn((4, 256, 14, 14), generator=gen)
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, 32, 0.5, 1, 1)
+    assert rel_err(dx, ref_dx) <= 1e-5
+    assert rel_err(dD, ref_dD) <= 1e-5
+    dx2, dD2, _, _ = _bwd(w, x, dy, 32, 0.5, 1, 1)
+    np.testing.assert_array_equal(dx, dx2)
+    np.testing.assert_array_equal(dD, dD2)
+
+
+def test_bwd_everything_pruned():
+    w, x = workloads.gen_integer_layer(seed=1, cout=32, cin=5, k=3, batch=1, H=6)
+    layer = onexn.prepare_layer(w, 16, 1.0, False)
+    dy = torch.ones((1, 32, 6, 6), device="cuda")
+    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, 32, 5, dy, (6, 6), 1, 1)
+    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, 32, 16, (3, 3), x.cuda(), dy, 1, 1)
+    torch.cuda.synchronize()
+    assert layer.t == 0 and dD.numel() == 0
+    assert torch.all(dx == 0)
