@@ -262,6 +262,78 @@ def mask_bench(wl, dev, reps):
         "per_layer": rows}), flush=True)
 
 
+def backward_bench(wl, dev, reps):
+    """Times one backward pass (onexn_conv2d_bwd_data and onexn_conv2d_bwd_weight
+    on every layer) with HIP events, after checking one layer's gradients
+    against the oracle at sampled entries.  Each of the two gradients does the
+    forward's actual flops (2 * pixels * N * kh * kw * t)."""
+    import oracle
+    stream = torch.cuda.current_stream(dev)
+    rows, t_sum, f_sum, troof = [], 0.0, 0.0, 0.0
+    peak = PEAK_TFLOPS[wl.dtype]
+    for li, layer in enumerate(wl.layers):
+        w, x = workloads.gen_layer(layer, wl.batch, wl.dtype)
+        packed = onexn.prepare_layer(w, layer.N, layer.p, layer.rearrange, dev)
+        gen = torch.Generator().manual_seed(layer.seed + 7)
+        dy = torch.randn((wl.batch, layer.cout, layer.Ho, layer.Ho), generator=gen).to(_TDT[wl.dtype])
+        xd, dyd = x.to(dev), dy.to(dev)
+        kk = (layer.k, layer.k)
+
+        def run():
+            dx = onexn.conv2d_bwd_data(packed.P, packed.I, packed.D, layer.cout, layer.cin, dyd,
+                                       (layer.H, layer.H), layer.stride, layer.pad)
+            dD = onexn.conv2d_bwd_weight(packed.P, packed.I, layer.cout, layer.N, kk, xd, dyd,
+                                         layer.stride, layer.pad)
+            return dx, dD
+        dx, dD = run()
+        torch.cuda.synchronize()
+        if li == 0:
+            # Parity before timing: sampled dX entries and every dD entry of the
+            # first 8 kept blocks against the oracle on the first image.
+            pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+            x0, dy0 = x[:1].double().numpy(), dy[:1].double().numpy()
+            ref_dx = oracle.conv2d_bwd_data(dy0, pr.wbar, (layer.H, layer.H), (layer.stride,) * 2,
+                                            (layer.pad,) * 2)
+            dx1 = onexn.conv2d_bwd_data(packed.P, packed.I, packed.D, layer.cout, layer.cin, dyd[:1].contiguous(),
+                                        (layer.H, layer.H), layer.stride, layer.pad)
+            dD1 = onexn.conv2d_bwd_weight(packed.P, packed.I, layer.cout, layer.N, kk, xd[:1].contiguous(),
+                                          dyd[:1].contiguous(), layer.stride, layer.pad)
+            torch.cuda.synchronize()
+            dw = oracle.conv2d_bwd_weight(x0, dy0, pr.T, layer.N, kk, (layer.stride,) * 2, (layer.pad,) * 2)
+            _, _, ref_dD = oracle.pack(dw, pr.T, layer.N)
+            bar = 2e-2 if wl.dtype == "bf16" else 1e-5
+
+            def rel(a, b):
+                return float(abs(a - b).max() / max(abs(b).max(), 1e-300))
+            e1 = rel(dx1.double().cpu().numpy(), ref_dx)
+            e2 = rel(dD1.double().cpu().numpy(), ref_dD)
+            if not (e1 <= bar and e2 <= bar):
+                print(json.dumps({"parity": "FAIL", "layer": layer.name, "dx": e1, "dD": e2}), flush=True)
+                sys.exit(3)
+        for _ in range(2):
+            run()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tl = e0.elapsed_time(e1) / reps / 1e3
+        fa = 2.0 * 2.0 * layer.out_pixels(wl.batch) * layer.N * layer.k * layer.k * packed.t
+        rows.append({"layer": layer.name, "us": round(tl * 1e6, 1), "gflop": round(fa / 1e9, 3),
+                     "tflops": round(fa / tl / 1e12, 3)})
+        t_sum, f_sum, troof = t_sum + tl, f_sum + fa, troof + fa / (peak * 1e12)
+        del dx, dD, xd, dyd
+    print(json.dumps({
+        "metric": "1xN sparse conv backward (input and kept-block weight gradients): TFLOP/s",
+        "value": round(f_sum / t_sum / 1e12, 3), "unit": "TFLOP/s", "higher_is_better": True, "n_gpus": 1,
+        "dtype": wl.dtype, "config": {"workload": wl.name, "layers": len(wl.layers), "batch": wl.batch},
+        "ms_per_pass": round(t_sum * 1e3, 3),
+        "roofline": {"bound": "mfma", "achieved": round(f_sum / t_sum / 1e12, 3), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(troof / t_sum, 4), "traffic": None},
+        "per_layer": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -272,6 +344,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--cpu-single-budget", type=float, default=8.0,
                     help="seconds of single-threaded oracle work")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward kernels on the workload's layers instead of the forward")
     ap.add_argument("--mask", action="store_true",
                     help="time the GPU mask building of the workload's layers instead of the conv")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -293,6 +367,9 @@ def main():
     wl = WORKLOADS[args.workload]()
     if args.mask:
         mask_bench(wl, dev, max(args.steps, 5))
+        return
+    if args.backward:
+        backward_bench(wl, dev, max(min(args.steps, 10), 2))
         return
     batch = wl.batch
     odt = _TDT[wl.out_dtype]

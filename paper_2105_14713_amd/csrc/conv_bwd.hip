@@ -20,9 +20,9 @@
 // the output pixel whose window puts that tap on it (when the stride
 // divides), weights being wave-uniform loads.
 //
-// bwd_weight.  A workgroup per kept block z.  Lanes split the output pixels;
-// for each tap a lane keeps N partial sums (one per block row) over its
-// pixels, then an LDS tree adds the 256 lanes' sums in a fixed order.  Both
+// bwd_weight.  A workgroup per (kept block z, tap).  Lanes split the output
+// pixels and keep N partial sums (one per block row) over their pixels, then
+// an LDS tree adds the 256 lanes' sums in a fixed order.  Both
 // kernels accumulate in fp32 and their results do not depend on timing.
 
 #include "conv_common.h"
@@ -124,6 +124,7 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_weight(ConvArgs a, const TX* 
     __shared__ float sR[kBwdThreads * N];
     const int tid = threadIdx.x;
     const int32_t z = blockIdx.x;
+    const int32_t q = blockIdx.y / a.kw, r = blockIdx.y - q * a.kw;
     // Col-group of block z: the last g with P[g] <= z (P clamped to [0, t]).
     int32_t lo = 0, hi = a.G - 1;
     while (lo < hi) {
@@ -138,8 +139,8 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_weight(ConvArgs a, const TX* 
     const int64_t HW = int64_t(a.H) * a.W;
     const int32_t KK = a.kh * a.kw;
 
-    for (int32_t q = 0; q < a.kh; ++q)
-        for (int32_t r = 0; r < a.kw; ++r) {
+    {
+        {
             float acc[N];
 #pragma unroll
             for (int i = 0; i < N; ++i) acc[i] = 0.f;
@@ -167,8 +168,8 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_weight(ConvArgs a, const TX* 
                 __syncthreads();
             }
             if (tid < N) dD[(int64_t(z) * N + tid) * KK + q * a.kw + r] = sR[tid * kBwdThreads];
-            __syncthreads();
         }
+    }
 }
 
 onexn_status check_common(const int32_t* P, int32_t n, int32_t m, int32_t kh, int32_t kw, int32_t N,
@@ -233,7 +234,7 @@ onexn_status launch_bwd_data(const ConvArgs& a, int32_t batch, const void* dy, v
 template <typename TX>
 onexn_status launch_bwd_weight(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
     auto go = [&](auto kern) {
-        hipLaunchKernelGGL(kern, dim3(uint32_t(a.t)), dim3(kBwdThreads), 0, s, a, static_cast<const TX*>(x),
+        hipLaunchKernelGGL(kern, dim3(uint32_t(a.t), uint32_t(a.KK)), dim3(kBwdThreads), 0, s, a, static_cast<const TX*>(x),
                            static_cast<const TX*>(dy), dD);
         return launched("conv2d_bwd_weight");
     };
