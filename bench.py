@@ -350,6 +350,8 @@ def main():
                     help="time the GPU mask building of the workload's layers instead of the conv")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a copy kernel of known size (for scaling byte counters)")
+    ap.add_argument("--tune", action="append", default=[], metavar="NAME=VALUE",
+                    help="a kernel-choice override of the library (onexn_set_tuning), for A/B timing")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the 1xN conv path here is single-GPU "
@@ -361,6 +363,9 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    for kv in args.tune:
+        name, _, value = kv.partition("=")
+        onexn.set_tuning(name, int(value))
     if args.copy_calibration:
         copy_calibration(dev)
         return
@@ -552,6 +557,8 @@ def main():
         "host_enqueued_ahead": host_ahead,
         "host_launch_us_per_step": round(host_step_s * 1e6, 1),
     }
+    if args.tune:
+        rec["config"]["tuning"] = args.tune
     if not args.no_cpu:
         print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl.layers, batch, wl, args.cpu_budget,

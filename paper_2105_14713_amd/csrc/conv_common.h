@@ -205,6 +205,8 @@ bool pw_tile_applies(const ConvArgs& a);
 onexn_status launch_pw_tile(ConvArgs a, hipStream_t stream);
 bool pw_bf16r_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 onexn_status launch_pw_bf16r(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
+bool pw_bf16s_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_pw_bf16s(ConvArgs a, onexn_dtype ydt, hipStream_t stream);
 bool kxk_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 bool pw_fma_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 bool pw_direct_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);

@@ -27,7 +27,7 @@ namespace {
 std::atomic<int32_t> g_tuning[kTuneCount];
 const char* const kTuneNames[kTuneCount] = {
     "kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw",
-    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp"};
+    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs"};
 
 }  // namespace
 
@@ -124,7 +124,18 @@ onexn_status conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* 
         a.y_pix = n;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (pw_bf16r_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_bf16r(a, ydt, s);
+    // bf16 1x1 N = 32 layers: the LDS-staged kernel for long contractions
+    // (2048 -> 2048 at 14x14, batch 256: 313 us against 360 us register-
+    // gathered), the register-gathered one otherwise.  The pwb_kernel tuning
+    // forces 1: register-gathered, 2: staged (an error where it does not fit).
+    if (!generic_forced()) {
+        const int32_t pbk = tuning(kTunePwbKernel);
+        const bool staged = pw_bf16s_applies(a, xdt, ydt, layout);
+        if (pbk == 2 && !staged)
+            return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_fwd: the LDS-staged bf16 kernel does not fit this layer");
+        if (staged && (pbk == 2 || (pbk != 1 && a.m >= 512))) return launch_pw_bf16s(a, ydt, s);
+        if (pw_bf16r_applies(a, xdt, ydt, layout)) return launch_pw_bf16r(a, ydt, s);
+    }
     // fp32 1x1 layers: the resident-tile kernel for stride-1 layers that
     // widen the channels over many pixels, the register-operand kernel for
     // the rest (contractions at least as long as the output is wide, few

@@ -31,6 +31,8 @@ enum Tune : int {
     kTuneFmaTile,      // 1x1 FMA: tile shape 1-5
     kTuneKxkSplit,     // k x k: workgroups per CU of the balanced split (0: none)
     kTuneKxkTp,        // k x k: tile capacity in pixels (128, 256)
+    kTunePwbKernel,    // bf16 1x1 N = 32: 1 register-gathered, 2 LDS-staged
+    kTunePwbWgs,       // LDS-staged bf16 1x1: workgroups
     kTuneCount
 };
 constexpr int32_t kTuneAuto = -1;

@@ -29,7 +29,8 @@ KINDS = {
     "kxk_stem": (7, 2, 3, 32, 3, torch.float32, 30, {}),
     "tile": (1, 1, 0, 16, 200, torch.float32, 12, {"pw_kernel": 1}),
     "direct": (1, 2, 0, 32, 90, torch.float32, 12, {"pw_kernel": 3}),
-    "bf16r": (1, 1, 0, 32, 96, torch.bfloat16, 12, {}),
+    "bf16r": (1, 1, 0, 32, 96, torch.bfloat16, 12, {"pwb_kernel": 1}),
+    "bf16s": (1, 1, 0, 32, 300, torch.bfloat16, 14, {"pwb_kernel": 2}),
     "generic_mfma": (5, 1, 2, 16, 30, torch.float32, 12, {}),
     "generic_fma": (3, 1, 1, 4, 30, torch.float32, 12, {}),
     "pw_fma": (1, 1, 0, 8, 30, torch.float32, 12, {}),

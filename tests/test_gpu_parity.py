@@ -156,14 +156,15 @@ def test_edge_shapes_integer_exact(case):
 
 
 @pytest.mark.parametrize("k,N,dt", [(1, 16, "f32"), (1, 32, "f32"), (3, 16, "f32"), (1, 4, "f32"),
-                                    (1, 32, "bf16")])
-def test_out_of_range_channels_are_skipped(k, N, dt):
+                                    (1, 32, "bf16"), (1, 32, "bf16s")])
+def test_out_of_range_channels_are_skipped(k, N, dt, tune):
     """Entries of I outside [0, m) contribute nothing (kept ascending, so the
     rest of the col-group is unaffected); P is clamped to [0, t]."""
     print(f"skip case k={k} N={N} {dt}", flush=True)
-    H = 10 if dt == "bf16" else 9       # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernel
+    H = 9 if dt == "f32" else 10        # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernels
+    tune("pwb_kernel", 2 if dt == "bf16s" else 1)
     w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=H)
-    if dt == "bf16":
+    if dt != "f32":
         w, x = w.bfloat16(), x.bfloat16()
     layer = onexn.prepare_layer(w, N, 0.5, False)
     P, I, D = layer.P.cpu(), layer.I.cpu().clone(), layer.D.cpu().clone()
@@ -241,8 +242,10 @@ def test_config1_full_size_sampled():
     _check_sampled(wl.layers[0], wl.batch, "f32", "f32", y, pr, x)
 
 
+@pytest.mark.parametrize("kernel", ["gathered", "staged"])
 @pytest.mark.parametrize("out_dtype", ["bf16", "f32"])
-def test_config4_full_size_sampled(out_dtype):
+def test_config4_full_size_sampled(out_dtype, kernel, tune):
+    tune("pwb_kernel", 1 if kernel == "gathered" else 2)
     wl = workloads.config4(out_dtype)
     y, pr, x = _run_layer(wl.layers[0], wl.batch, "bf16", out_dtype)
     _check_sampled(wl.layers[0], wl.batch, "bf16", out_dtype, y, pr, x)
@@ -316,7 +319,8 @@ def test_pw_tile_variants_integer_exact(N, groups, m, hw, wgs, tune):
         np.testing.assert_array_equal(y, ref)
 
 
-@pytest.mark.parametrize("variant", ["g4rp2", "g4rp4", "g4rp6", "g8rp1", "g8rp2"])
+@pytest.mark.parametrize("variant", ["g4rp2", "g4rp4", "g4rp6", "g8rp1", "g8rp2", "staged",
+                                     "staged_w1", "staged_w3"])
 @pytest.mark.parametrize("shape", [
     dict(m=300, B=3, H=14, W=14),    # 5 channel chunks (ragged last), partial last granule per image
     dict(m=64, B=2, H=12, W=12),     # one chunk, whole granules, tiles across images
@@ -328,14 +332,26 @@ def test_pw_bf16_integer_exact(shape, variant, tune):
     """The bf16 pointwise kernel (1x1, N = 32, pixels per image a multiple of
     4): the register-gathered kernel with 4-pixel granules at pipeline depths
     2, 4, 6 and with 8-pixel granules at depths 1, 2 (images of 12 and 196
-    pixels end in a half-duplicate granule); more input channels than it
-    stages (m = 2100) take the generic kernel.  Small integers are exact in
-    bf16 and in fp32 accumulation, so fp32 output is bit-exact and bf16 output
-    equals the oracle rounded to bf16.  Covers ragged col-groups and a partial
-    last set of 8 col-groups (n = 304) and dense to nearly empty col-groups
-    (p = 0, 0.5, 0.97)."""
-    tune("pwb_gp", variant[1])
-    tune("pwb_rp", variant[4:])
+    pixels end in a half-duplicate granule), where more input channels than
+    it stages (m = 2100) take the generic kernel; and the LDS-staged kernel
+    (any m; images of 12 and 196 pixels end in a half-filled granule) on its
+    default grid and on grids of 1 and 3 workgroups, which walk several work
+    items each (the chunk ring runs on across items, and the next item's
+    first windows are loaded before the stores).  At p = 0.97 a window of 16
+    kept blocks spans more than two 128-channel chunks and is multiplied in
+    several passes.  Small integers are exact in bf16 and in fp32
+    accumulation, so fp32 output is bit-exact and bf16 output equals the
+    oracle rounded to bf16.  Covers ragged col-groups, a partial last set of
+    col-groups (n = 304: 8 per set gathered, 15 per set staged) and dense to
+    nearly empty col-groups (p = 0, 0.5, 0.97)."""
+    if variant.startswith("staged"):
+        tune("pwb_kernel", 2)
+        if "_w" in variant:
+            tune("pwb_wgs", variant.split("_w")[1])
+    else:
+        tune("pwb_kernel", 1)
+        tune("pwb_gp", variant[1])
+        tune("pwb_rp", variant[4:])
     c = shape
     n = 9 * 32 + 16
     w, x = workloads.gen_integer_layer(seed=c["m"] + int(c["B"]), cout=n, cin=c["m"], k=1,
@@ -436,17 +452,19 @@ def test_kxk_matches_generic_on_random_fp32():
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "generic", "fma", "pwfma", "direct"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "bf16s", "generic", "fma", "pwfma", "direct"])
 def test_reads_stay_inside_I_and_D(kind, tune):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
     t would put NaN into the output."""
     k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
-                      "bf16": (1, 32, 96, torch.bfloat16, 12),
+                      "bf16": (1, 32, 96, torch.bfloat16, 12), "bf16s": (1, 32, 300, torch.bfloat16, 12),
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
                       "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
     if kind in ("tile", "direct"):
         tune("pw_kernel", {"tile": 1, "direct": 3}[kind])
+    if kind in ("bf16", "bf16s"):
+        tune("pwb_kernel", 1 if kind == "bf16" else 2)
     n = 3 * N + N // 2
     w, x = workloads.gen_integer_layer(seed=7, cout=n, cin=m, k=k, batch=2, H=H, wmax=2, xmax=2)
     w, x = w.to(dt), x.to(dt)
