@@ -27,7 +27,7 @@ namespace {
 std::atomic<int32_t> g_tuning[kTuneCount];
 const char* const kTuneNames[kTuneCount] = {
     "kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw",
-    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs"};
+    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs", "kxkf_split"};
 
 }  // namespace
 
@@ -155,6 +155,7 @@ onexn_status conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* 
     }
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
+    if (kxk_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk_fma(a, s);
     return launch_generic(a, xdt, ydt, s);
 }
 

@@ -32,7 +32,9 @@ KINDS = {
     "bf16r": (1, 1, 0, 32, 96, torch.bfloat16, 12, {"pwb_kernel": 1}),
     "bf16s": (1, 1, 0, 32, 300, torch.bfloat16, 14, {"pwb_kernel": 2}),
     "generic_mfma": (5, 1, 2, 16, 30, torch.float32, 12, {}),
-    "generic_fma": (3, 1, 1, 4, 30, torch.float32, 12, {}),
+    "kxk_fma": (3, 1, 1, 4, 30, torch.float32, 12, {}),
+    "kxk_fma_split": (3, 1, 1, 8, 30, torch.float32, 12, {"kxkf_split": 4}),
+    "generic_fma": (5, 1, 2, 4, 30, torch.float32, 12, {}),
     "pw_fma": (1, 1, 0, 8, 30, torch.float32, 12, {}),
     "bf16_kxk": (3, 1, 1, 16, 24, torch.bfloat16, 10, {}),
 }

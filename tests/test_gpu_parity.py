@@ -156,7 +156,7 @@ def test_edge_shapes_integer_exact(case):
 
 
 @pytest.mark.parametrize("k,N,dt", [(1, 16, "f32"), (1, 32, "f32"), (3, 16, "f32"), (1, 4, "f32"),
-                                    (1, 32, "bf16"), (1, 32, "bf16s")])
+                                    (3, 4, "f32"), (1, 32, "bf16"), (1, 32, "bf16s")])
 def test_out_of_range_channels_are_skipped(k, N, dt, tune):
     """Entries of I outside [0, m) contribute nothing (kept ascending, so the
     rest of the col-group is unaffected); P is clamped to [0, t]."""
@@ -366,6 +366,30 @@ def test_pw_bf16_integer_exact(shape, variant, tune):
         np.testing.assert_array_equal(yb, refb)
 
 
+@pytest.mark.parametrize("split", ["1", "4"])
+@pytest.mark.parametrize("case", [
+    dict(N=4, m=64, n=64, B=1, H=56, W=56, s=1, pd=1),    # the 3x3 N = 4 batch-1 workload's shape
+    dict(N=1, m=13, n=5, B=3, H=19, W=17, s=1, pd=1),     # odd sizes, pixel blocks across images
+    dict(N=2, m=30, n=9, B=2, H=15, W=13, s=2, pd=1),     # stride 2
+    dict(N=8, m=21, n=28, B=2, H=12, W=11, s=1, pd=0),    # no padding, ragged last col-group
+    dict(N=8, m=300, n=16, B=1, H=7, W=7, s=1, pd=1),     # long contraction, few pixels
+    dict(N=4, m=7, n=12, B=4, H=9, W=10, s=3, pd=2),      # stride 3, padding 2
+], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
+def test_kxk_fma_integer_exact(case, split, tune):
+    """The 3x3 FMA kernel (N <= 8) with four col-groups per workgroup and with
+    the contraction split over the four waves, p from dense to nearly empty
+    (odd and single kept blocks at the end of a share)."""
+    tune("kxkf_split", split)
+    c = case
+    w, x = workloads.gen_integer_layer(seed=c["m"] * 3 + c["N"], cout=c["n"], cin=c["m"], k=3,
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=2, xmax=2)
+    print(f"kxk fma {c} split={split}", flush=True)
+    for p in (0.0, 0.5, 0.95):
+        y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        np.testing.assert_array_equal(y, ref)
+
+
 @pytest.mark.parametrize("tp", ["128", "256"])
 @pytest.mark.parametrize("case", [
     dict(k=3, s=1, pd=1, B=2, H=56, W=56, m=20, N=32),   # 4 whole rows per tile
@@ -452,7 +476,7 @@ def test_kxk_matches_generic_on_random_fp32():
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "bf16s", "generic", "fma", "pwfma", "direct"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "bf16s", "generic", "fma", "fma5", "pwfma", "direct"])
 def test_reads_stay_inside_I_and_D(kind, tune):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
@@ -460,6 +484,7 @@ def test_reads_stay_inside_I_and_D(kind, tune):
     k, N, m, dt, H = {"kxk": (3, 32, 40, torch.float32, 12), "tile": (1, 16, 200, torch.float32, 12),
                       "bf16": (1, 32, 96, torch.bfloat16, 12), "bf16s": (1, 32, 300, torch.bfloat16, 12),
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
+                      "fma5": (5, 4, 30, torch.float32, 12),
                       "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
     if kind in ("tile", "direct"):
         tune("pw_kernel", {"tile": 1, "direct": 3}[kind])
