@@ -60,6 +60,9 @@ for _N in (4, 8, 16, 32):
 for _N in (4, 32):
     for _lay in ("rows", "cols"):
         WORKLOADS[f"fc_n{_N}_{_lay}"] = (lambda N=_N, lay=_lay: workloads.fc_resnet50(N, lay))
+WORKLOADS["c1_nhwc"] = lambda: workloads.nhwc(workloads.config1())
+for _N in (16, 32):
+    WORKLOADS[f"c3_n{_N}_p50_nhwc"] = (lambda N=_N: workloads.nhwc(workloads.config3(N, 0.5)))
 
 _ESIZE = {"f32": 4, "bf16": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -140,6 +143,8 @@ def parity_gate(prepared, wl):
         y = ys[0]
         if wl.fc_layout == "cols":        # [n][batch] -> [batch][n]
             y = y.t().contiguous()
+        if wl.layout == "nhwc":           # [batch][Ho][Wo][n] -> [batch][n][Ho][Wo]
+            y = y.permute(0, 3, 1, 2).contiguous()
         y = y.reshape(x_cpu.shape[0], layer.cout, layer.Ho, layer.Ho)
         idx = workloads.sample_outputs(tuple(y.shape), layer.N, PARITY_SAMPLES, seed=li)
         got = y.reshape(-1)[torch.from_numpy(idx).to(y.device)].double().cpu().numpy()
@@ -408,8 +413,12 @@ def main():
             xd = (x2 if wl.fc_layout == "rows" else x2.t().contiguous()).to(dev)
             yshape = (batch, layer.cout) if wl.fc_layout == "rows" else (layer.cout, batch)
         else:
-            xd = x.to(dev)
-            yshape = (batch, layer.cout, Ho, Ho)
+            if wl.layout == "nhwc":
+                xd = x.permute(0, 2, 3, 1).contiguous().to(dev)
+                yshape = (batch, Ho, Ho, layer.cout)
+            else:
+                xd = x.to(dev)
+                yshape = (batch, layer.cout, Ho, Ho)
         xs = [xd] + [xd.clone() for _ in range(copies - 1)]
         ys = [torch.empty(yshape, dtype=odt, device=dev) for _ in range(copies)]
         if wl.fc_layout:
@@ -418,7 +427,7 @@ def main():
                      for r in range(copies)]
         else:
             calls = [onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
-                                     layer.stride, layer.pad, "nchw", stream.cuda_stream)
+                                     layer.stride, layer.pad, wl.layout, stream.cuda_stream)
                      for r in range(copies)]
         prepared.append((layer, packed, xs, ys, w, x, calls))
 
@@ -534,7 +543,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.description, "batch": batch,
                    "layers": len(wl.layers), "out_dtype": wl.out_dtype,
-                   "layout": wl.fc_layout or "nchw"},
+                   "layout": wl.fc_layout or wl.layout},
         "dense_equiv_tflops": round(f_dense * args.steps / (total_ms / 1e3) / 1e12, 3),
         "hbm_gbps": round(b_alg * args.steps / (total_ms / 1e3) / 1e9, 1),
         "kernel_us": {"mean": round(avg_step_ms * 1e3, 2), "p10": round(per_step[len(per_step) // 10] * 1e3, 2),

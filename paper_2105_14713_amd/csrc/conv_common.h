@@ -213,6 +213,8 @@ bool pw_direct_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onex
 onexn_status launch_pw_direct(ConvArgs a, hipStream_t stream);
 onexn_status launch_pw_fma(ConvArgs a, hipStream_t stream);
 bool kxk_fma_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+bool pw_nhwc_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+onexn_status launch_pw_nhwc(ConvArgs a, hipStream_t stream);
 onexn_status launch_kxk_fma(ConvArgs a, hipStream_t stream);
 onexn_status launch_kxk(ConvArgs a, hipStream_t stream);
 

@@ -156,6 +156,7 @@ onexn_status conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const void* 
     if (kxk_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk(a, s);
     if (pw_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_fma(a, s);
     if (kxk_fma_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_kxk_fma(a, s);
+    if (pw_nhwc_applies(a, xdt, ydt, layout) && !generic_forced()) return launch_pw_nhwc(a, s);
     return launch_generic(a, xdt, ydt, s);
 }
 

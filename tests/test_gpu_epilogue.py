@@ -74,17 +74,20 @@ def test_epilogue_integer_exact(kind, act, tune):
         np.testing.assert_array_equal(y.double().cpu().numpy(), want)
 
 
-def test_epilogue_nhwc_and_partial_parameters():
-    """NHWC layout; scale alone, bias alone."""
-    w, x = workloads.gen_integer_layer(seed=3, cout=40, cin=17, k=3, batch=2, H=9, wmax=2, xmax=2)
+@pytest.mark.parametrize("k,N", [(3, 16), (1, 16), (1, 32)])
+def test_epilogue_nhwc_and_partial_parameters(k, N):
+    """NHWC layout (3x3: the generic kernel; 1x1: the NHWC kernel); scale
+    alone, bias alone."""
+    w, x = workloads.gen_integer_layer(seed=3, cout=40, cin=17, k=k, batch=2, H=9, wmax=2, xmax=2)
     scale, bias = _params(40, 5)
-    layer = onexn.prepare_layer(w, 16, 0.5, True)
-    pr = oracle.prune(w.double().numpy(), 16, 0.5, True)
-    conv = oracle.conv2d(x.double().numpy(), pr.wbar, (1, 1), (1, 1))
+    layer = onexn.prepare_layer(w, N, 0.5, True)
+    pr = oracle.prune(w.double().numpy(), N, 0.5, True)
+    pd = k // 2
+    conv = oracle.conv2d(x.double().numpy(), pr.wbar, (1, 1), (pd, pd))
     xh = x.permute(0, 2, 3, 1).contiguous().cuda()
     sp, bp = scale[layer.perm.long()], bias[layer.perm.long()]
     for sc, bi in ((sp, None), (None, bp), (sp, bp)):
-        y = layer.forward(xh, 1, 1, "nhwc", scale=None if sc is None else sc.cuda(),
+        y = layer.forward(xh, 1, pd, "nhwc", scale=None if sc is None else sc.cuda(),
                           bias=None if bi is None else bi.cuda(), act="relu")
         torch.cuda.synchronize()
         ref = oracle.epilogue(conv, None if sc is None else sc.double().numpy(),

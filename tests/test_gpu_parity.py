@@ -156,22 +156,26 @@ def test_edge_shapes_integer_exact(case):
 
 
 @pytest.mark.parametrize("k,N,dt", [(1, 16, "f32"), (1, 32, "f32"), (3, 16, "f32"), (1, 4, "f32"),
-                                    (3, 4, "f32"), (1, 32, "bf16"), (1, 32, "bf16s")])
+                                    (3, 4, "f32"), (1, 32, "bf16"), (1, 32, "bf16s"), (1, 32, "nhwc")])
 def test_out_of_range_channels_are_skipped(k, N, dt, tune):
     """Entries of I outside [0, m) contribute nothing (kept ascending, so the
     rest of the col-group is unaffected); P is clamped to [0, t]."""
     print(f"skip case k={k} N={N} {dt}", flush=True)
-    H = 9 if dt == "f32" else 10        # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernels
+    H = 10 if dt.startswith("bf16") else 9   # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernels
     tune("pwb_kernel", 2 if dt == "bf16s" else 1)
     w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=H)
-    if dt != "f32":
+    if dt.startswith("bf16"):
         w, x = w.bfloat16(), x.bfloat16()
+    nhwc = dt == "nhwc"
+    xin = (x.permute(0, 2, 3, 1).contiguous() if nhwc else x).cuda()
+    lay = "nhwc" if nhwc else "nchw"
+    back = (lambda t: t.permute(0, 3, 1, 2)) if nhwc else (lambda t: t)
     layer = onexn.prepare_layer(w, N, 0.5, False)
     P, I, D = layer.P.cpu(), layer.I.cpu().clone(), layer.D.cpu().clone()
     hi, lo = int(P[1]) - 1, int(P[1])          # last entry of group 0, first of group 1
     I[hi], I[lo] = 1 << 20, -5
-    y = onexn.conv2d_fwd(layer.P, I.cuda(), layer.D, 4 * N, x.cuda(), 1, k // 2,
-                         out_dtype=torch.float32)
+    y = back(onexn.conv2d_fwd(layer.P, I.cuda(), layer.D, 4 * N, xin, 1, k // 2, lay,
+                              out_dtype=torch.float32))
     # Expected: the same arrays with those two entries' weights zeroed.
     D0 = D.clone()
     D0[hi] = 0
@@ -183,7 +187,7 @@ def test_out_of_range_channels_are_skipped(k, N, dt, tune):
     np.testing.assert_array_equal(y.double().cpu().numpy(), ref)
     Pbad = layer.P.clone()
     Pbad[-1] = 1 << 30
-    y2 = onexn.conv2d_fwd(Pbad, layer.I, layer.D, 4 * N, x.cuda(), 1, k // 2)
+    y2 = onexn.conv2d_fwd(Pbad, layer.I, layer.D, 4 * N, xin, 1, k // 2, lay)
     torch.cuda.synchronize()
     assert torch.isfinite(y2).all()
 
@@ -390,6 +394,29 @@ def test_kxk_fma_integer_exact(case, split, tune):
         np.testing.assert_array_equal(y, ref)
 
 
+@pytest.mark.parametrize("case", [
+    dict(N=32, m=64, n=80, B=2, H=12, W=12, s=1, pd=0),     # one tile per 32 pixels, ragged last col-group
+    dict(N=16, m=13, n=40, B=3, H=9, W=7, s=1, pd=0),       # pixel tiles across images, odd sizes
+    dict(N=32, m=300, n=300, B=2, H=14, W=14, s=2, pd=0),   # stride 2 (downsample), 38 col-groups (5 sets)
+    dict(N=16, m=150, n=64, B=1, H=10, W=11, s=2, pd=1),    # padding: input pixels outside the image
+    dict(N=32, m=1100, n=64, B=1, H=7, W=7, s=1, pd=0),     # long rows, several index windows
+    dict(N=16, m=1100, n=48, B=2, H=5, W=6, s=1, pd=0),     # N = 16 with one column block per tile
+    dict(N=32, m=45, n=33, B=4, H=3, W=5, s=1, pd=0),       # n not a multiple of 4 (scalar stores)
+], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
+def test_pw_nhwc_integer_exact(case):
+    """The NHWC 1x1 kernel (input rows of a pixel tile staged in LDS, shared by
+    eight col-groups): strides, padding, ragged col-groups and pixel tiles,
+    rows longer than one index window, and p from dense to nearly empty."""
+    c = case
+    w, x = workloads.gen_integer_layer(seed=c["m"] + c["N"] + c["s"], cout=c["n"], cin=c["m"], k=1,
+                                       batch=c["B"], H=c["H"], W=c["W"], wmax=2, xmax=2)
+    print(f"pw nhwc {c}", flush=True)
+    for p in (0.0, 0.5, 0.95):
+        y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"], "nhwc")
+        ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
+        np.testing.assert_array_equal(y, ref)
+
+
 @pytest.mark.parametrize("tp", ["128", "256"])
 @pytest.mark.parametrize("case", [
     dict(k=3, s=1, pd=1, B=2, H=56, W=56, m=20, N=32),   # 4 whole rows per tile
@@ -476,7 +503,8 @@ def test_kxk_matches_generic_on_random_fp32():
     assert rel_err(y, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "bf16s", "generic", "fma", "fma5", "pwfma", "direct"])
+@pytest.mark.parametrize("kind", ["kxk", "tile", "bf16", "bf16s", "generic", "fma", "fma5", "pwfma", "direct",
+                                  "nhwc16", "nhwc32"])
 def test_reads_stay_inside_I_and_D(kind, tune):
     """I and D are views at the start of larger buffers whose tails hold a
     valid channel index (0) and NaN weights: a kernel that used any entry past
@@ -485,7 +513,8 @@ def test_reads_stay_inside_I_and_D(kind, tune):
                       "bf16": (1, 32, 96, torch.bfloat16, 12), "bf16s": (1, 32, 300, torch.bfloat16, 12),
                       "generic": (5, 16, 30, torch.float32, 12), "fma": (3, 4, 30, torch.float32, 12),
                       "fma5": (5, 4, 30, torch.float32, 12),
-                      "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12)}[kind]
+                      "pwfma": (1, 4, 30, torch.float32, 12), "direct": (1, 32, 90, torch.float32, 12),
+                      "nhwc16": (1, 16, 90, torch.float32, 12), "nhwc32": (1, 32, 90, torch.float32, 12)}[kind]
     if kind in ("tile", "direct"):
         tune("pw_kernel", {"tile": 1, "direct": 3}[kind])
     if kind in ("bf16", "bf16s"):
@@ -501,7 +530,11 @@ def test_reads_stay_inside_I_and_D(kind, tune):
     D_big = torch.full((t + extra, N, k, k), float("nan"), dtype=dt, device="cuda")
     D_big[:t] = layer.D
     pd = k // 2
-    y = onexn.conv2d_fwd(layer.P, I_big[:t], D_big[:t], n, x.cuda(), 1, pd, out_dtype=torch.float32)
+    if kind.startswith("nhwc"):
+        y = onexn.conv2d_fwd(layer.P, I_big[:t], D_big[:t], n, x.permute(0, 2, 3, 1).contiguous().cuda(),
+                             1, pd, "nhwc", out_dtype=torch.float32).permute(0, 3, 1, 2)
+    else:
+        y = onexn.conv2d_fwd(layer.P, I_big[:t], D_big[:t], n, x.cuda(), 1, pd, out_dtype=torch.float32)
     torch.cuda.synchronize()
     ref, _ = oracle_conv(w.float(), x.float(), N, 0.5, False, 1, pd)
     np.testing.assert_array_equal(y.double().cpu().numpy(), ref)

@@ -15,11 +15,11 @@ Generation: ``torch.Generator('cpu').manual_seed(seed)``; per layer the weight
 is drawn first, then the input, both in float32.  bf16 values come from the
 float32 draw by round-to-nearest-even (``Tensor.to(torch.bfloat16)``).
 """
-from .configs import (ConvLayer, Workload, all_workloads, config0, config1, config2, config3,
+from .configs import (ConvLayer, Workload, all_workloads, config0, config1, config2, config3, nhwc,
                       config4, fc_resnet50, mobilenet_v2_pointwise, resnet50_convs)
 from .gen import gen_activation, gen_integer_layer, gen_layer, gen_weight
 from .sampling import sample_outputs
 
-__all__ = ["ConvLayer", "Workload", "all_workloads", "config0", "config1", "config2", "config3",
+__all__ = ["ConvLayer", "Workload", "all_workloads", "config0", "config1", "config2", "config3", "nhwc",
            "config4", "fc_resnet50", "mobilenet_v2_pointwise", "resnet50_convs", "gen_activation",
            "gen_integer_layer", "gen_layer", "gen_weight", "sample_outputs"]

@@ -4,7 +4,7 @@ The networks are the ones the paper prunes (Sec. 4.1): ResNet-50 and
 MobileNet-V2 at 224x224 input.  Their trained weights and ImageNet inputs are
 not used; see the package docstring for the stand-ins.
 """
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import List, Tuple
 
 
@@ -40,6 +40,7 @@ class Workload:
     layers: Tuple[ConvLayer, ...] = field(default_factory=tuple)
     description: str = ""
     fc_layout: str = ""           # "rows" / "cols" for a fully connected layer, "" for convs
+    layout: str = "nchw"          # activation layout of the convs: "nchw" or "nhwc"
 
 
 def config0() -> Workload:
@@ -143,6 +144,14 @@ def fc_resnet50(N: int = 32, layout: str = "rows") -> Workload:
                     fc_layout=layout)
 
 
+def nhwc(wl: Workload) -> Workload:
+    """The same workload with NHWC activations ([batch][H][W][channels] in and
+    out): the gather of Eq. 8 then picks single values out of each pixel's row
+    of channels."""
+    return replace(wl, name=wl.name + "_nhwc", layout="nhwc",
+                   description=wl.description + ", NHWC activations")
+
+
 def all_workloads() -> List[Workload]:
     out = [config0(), config1(), config2()]
     for N in (4, 8, 16, 32):
@@ -150,4 +159,5 @@ def all_workloads() -> List[Workload]:
             out.append(config3(N, p))
     out += [config4("bf16"), config4("f32")]
     out += [fc_resnet50(N, lay) for N in (4, 32) for lay in ("rows", "cols")]
+    out += [nhwc(config1()), nhwc(config3(16, 0.5)), nhwc(config3(32, 0.5))]
     return out
