@@ -27,7 +27,8 @@ namespace {
 std::atomic<int32_t> g_tuning[kTuneCount];
 const char* const kTuneNames[kTuneCount] = {
     "kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw",
-    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs", "kxkf_split"};
+    "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs", "kxkf_split",
+    "nhwc_tile"};
 
 }  // namespace
 

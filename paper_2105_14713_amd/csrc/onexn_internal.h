@@ -34,6 +34,7 @@ enum Tune : int {
     kTunePwbKernel,    // bf16 1x1 N = 32: 1 register-gathered, 2 LDS-staged
     kTunePwbWgs,       // LDS-staged bf16 1x1: workgroups
     kTuneKxfSplit,     // 3x3 FMA (N <= 8): waves per unit (1, 4)
+    kTuneNhwcTile,     // NHWC 1x1: column blocks per tile
     kTuneCount
 };
 constexpr int32_t kTuneAuto = -1;

@@ -156,17 +156,20 @@ def test_edge_shapes_integer_exact(case):
 
 
 @pytest.mark.parametrize("k,N,dt", [(1, 16, "f32"), (1, 32, "f32"), (3, 16, "f32"), (1, 4, "f32"),
-                                    (3, 4, "f32"), (1, 32, "bf16"), (1, 32, "bf16s"), (1, 32, "nhwc")])
+                                    (3, 4, "f32"), (1, 32, "bf16"), (1, 32, "bf16s"), (1, 32, "nhwc"),
+                                    (1, 16, "nhwc_long")])
 def test_out_of_range_channels_are_skipped(k, N, dt, tune):
     """Entries of I outside [0, m) contribute nothing (kept ascending, so the
     rest of the col-group is unaffected); P is clamped to [0, t]."""
     print(f"skip case k={k} N={N} {dt}", flush=True)
     H = 10 if dt.startswith("bf16") else 9   # bf16 1x1 N=32 with H*W % 4 == 0: the bf16 pointwise kernels
     tune("pwb_kernel", 2 if dt == "bf16s" else 1)
-    w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=70, k=k, batch=2, H=H)
+    # (nhwc_long: col-groups longer than the NHWC kernel keeps in registers)
+    w, x = workloads.gen_integer_layer(seed=4, cout=4 * N, cin=300 if dt == "nhwc_long" else 70, k=k,
+                                       batch=2, H=H)
     if dt.startswith("bf16"):
         w, x = w.bfloat16(), x.bfloat16()
-    nhwc = dt == "nhwc"
+    nhwc = dt.startswith("nhwc")
     xin = (x.permute(0, 2, 3, 1).contiguous() if nhwc else x).cuda()
     lay = "nhwc" if nhwc else "nchw"
     back = (lambda t: t.permute(0, 3, 1, 2)) if nhwc else (lambda t: t)
@@ -394,23 +397,28 @@ def test_kxk_fma_integer_exact(case, split, tune):
         np.testing.assert_array_equal(y, ref)
 
 
+@pytest.mark.parametrize("tile", [None, "3", "16"])
 @pytest.mark.parametrize("case", [
-    dict(N=32, m=64, n=80, B=2, H=12, W=12, s=1, pd=0),     # one tile per 32 pixels, ragged last col-group
-    dict(N=16, m=13, n=40, B=3, H=9, W=7, s=1, pd=0),       # pixel tiles across images, odd sizes
-    dict(N=32, m=300, n=300, B=2, H=14, W=14, s=2, pd=0),   # stride 2 (downsample), 38 col-groups (5 sets)
+    dict(N=32, m=64, n=80, B=2, H=12, W=12, s=1, pd=0),     # 3 col-groups, 2 waves each; ragged last col-group
+    dict(N=16, m=13, n=40, B=3, H=9, W=7, s=1, pd=0),       # rows not a multiple of 4, tiles across images
+    dict(N=32, m=300, n=300, B=2, H=14, W=14, s=2, pd=0),   # stride 2, 10 col-groups (sets of 8 and 2)
     dict(N=16, m=150, n=64, B=1, H=10, W=11, s=2, pd=1),    # padding: input pixels outside the image
-    dict(N=32, m=1100, n=64, B=1, H=7, W=7, s=1, pd=0),     # long rows, several index windows
-    dict(N=16, m=1100, n=48, B=2, H=5, W=6, s=1, pd=0),     # N = 16 with one column block per tile
+    dict(N=32, m=400, n=64, B=1, H=7, W=7, s=1, pd=0),      # longest rows, several index windows
+    dict(N=16, m=390, n=48, B=2, H=5, W=6, s=1, pd=0),      # long rows not a multiple of 4
     dict(N=32, m=45, n=33, B=4, H=3, W=5, s=1, pd=0),       # n not a multiple of 4 (scalar stores)
+    dict(N=16, m=32, n=16, B=2, H=19, W=21, s=1, pd=0),     # one col-group shared by 8 waves
 ], ids=lambda c: f"N{c['N']}_m{c['m']}_n{c['n']}_B{c['B']}_{c['H']}x{c['W']}_s{c['s']}p{c['pd']}")
-def test_pw_nhwc_integer_exact(case):
+def test_pw_nhwc_integer_exact(case, tile, tune):
     """The NHWC 1x1 kernel (input rows of a pixel tile staged in LDS, shared by
-    eight col-groups): strides, padding, ragged col-groups and pixel tiles,
-    rows longer than one index window, and p from dense to nearly empty."""
+    up to eight col-groups) at several tile sizes: strides, padding, ragged
+    col-groups and tiles, col-groups held in registers and streamed (p from
+    dense to nearly empty), rows longer than one index window."""
+    if tile is not None:
+        tune("nhwc_tile", tile)
     c = case
     w, x = workloads.gen_integer_layer(seed=c["m"] + c["N"] + c["s"], cout=c["n"], cin=c["m"], k=1,
                                        batch=c["B"], H=c["H"], W=c["W"], wmax=2, xmax=2)
-    print(f"pw nhwc {c}", flush=True)
+    print(f"pw nhwc {c} tile={tile}", flush=True)
     for p in (0.0, 0.5, 0.95):
         y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"], "nhwc")
         ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
