@@ -63,36 +63,38 @@ constexpr int kNMaxBlocks = 64;          // column blocks per tile
 // LDS of a tile of P pixels: P rows of m + 1 floats, then P 8-byte offsets.
 int64_t nhwc_tile_bytes(int64_t P, int32_t m) { return (P * (m + 1) + (P & 1)) * 4 + P * 8; }
 
-// Stages the tile's P rows: granules of Q consecutive channels (Q divides m),
-// each thread's kNStageFloats / Q granules of a batch loaded before any is
-// written.
+// Stages the tile's P rows: granules of Q consecutive channels (Q divides m).
+// Per batch (kNStageFloats floats, or 16 single floats) a thread first reads
+// the row offsets, then issues every load (no branch between them: a granule
+// past the tile or of a zero row loads granule 0 and is dropped or zeroed),
+// then writes LDS.
 template <int Q>
 __device__ __forceinline__ void stage_rows(const ConvArgs& a, float* sxn, const int64_t* srco,
                                            int32_t P, int tid) {
     typedef typename VecF<Q>::T V;
-    constexpr int SB = kNStageFloats / Q;
+    constexpr int SB = Q == 1 ? 16 : kNStageFloats / Q;   // (single floats: registers for 16)
     const int32_t m = a.m, pitch = m + 1, gr = m / Q, total = P * gr;
     const V* __restrict__ x = static_cast<const V*>(a.x);
     for (int32_t e0 = 0; e0 < total; e0 += SB * kNThreads) {
-        V v[SB];
+        int64_t src[SB];
         int32_t d[SB];
 #pragma unroll
         for (int k = 0; k < SB; ++k) {
             const int32_t e = e0 + k * kNThreads + tid;
-            d[k] = -1;
-            if (e < total) {
-                const int32_t r = e / gr, c = e - r * gr;
-                const int64_t src = srco[r];
-                d[k] = r * pitch + c * Q;
-                if (src >= 0) v[k] = x[src / Q + c];
-                else v[k] = V(0.f);
-            }
+            const int32_t ec = e < total ? e : total - 1;
+            const int32_t r = ec / gr, c = ec - r * gr;
+            const int64_t s = srco[r];
+            d[k] = e < total ? r * pitch + c * Q : -1;
+            src[k] = s >= 0 ? s / Q + c : -1;
         }
+        V v[SB];
+#pragma unroll
+        for (int k = 0; k < SB; ++k) v[k] = x[src[k] >= 0 ? src[k] : 0];
 #pragma unroll
         for (int k = 0; k < SB; ++k)
             if (d[k] >= 0) {
 #pragma unroll
-                for (int q = 0; q < Q; ++q) sxn[d[k] + q] = vec_el<Q>(v[k], q);
+                for (int q = 0; q < Q; ++q) sxn[d[k] + q] = src[k] >= 0 ? vec_el<Q>(v[k], q) : 0.f;
             }
     }
 }
