@@ -226,6 +226,15 @@ onexn_status launch_n(ConvArgs a, hipStream_t s) {
     };
     int choice = 0;
     if (tuning(kTuneDirectTile) >= 0) choice = tuning(kTuneDirectTile);
+    // Widening layers with many col-groups and few pixels (the 14x14 and 7x7
+    // expansions of MobileNet-V2, 64->384 to 160->960) run faster with two
+    // waves per unit: 34.6 -> 28.2 us and 48 -> 43 us per layer in the
+    // whole-step timing at N = 32, batch 128.  (Per-layer sweeps suggested
+    // other shapes for more layers, ResNet-50's strided ones among them; in
+    // whole steps those measured slower, up to 23 us per layer, and keep the
+    // rule below.)
+    if (choice == 0 && N == 32 && a.n > a.m && a.G >= 8 && a.npix <= 32768 && a.sh == 1 && a.sw == 1)
+        choice = 3;
     if (choice == 0) {
         if (wgs(2, 1) >= want || avg_kept < 64) choice = 1;
         else if (wgs(1, 1) >= want || avg_kept < 128) choice = 2;
