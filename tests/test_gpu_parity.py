@@ -294,6 +294,40 @@ def test_config3_mobilenet_v2_layer_sampled(li):
             assert rel_err(got, ref) <= 1e-5, (base.name, N, p)
 
 
+@pytest.mark.parametrize("li", range(len(_MB)), ids=[l.name for l in _MB])
+def test_config3_mobilenet_v2_layer_sampled_nhwc(li):
+    """The MobileNet-V2 layers with NHWC activations at full size (batch 128),
+    N = 16 and 32 at p = 0.5: the NHWC 1x1 kernel in the launch configuration
+    the benchmark times, on >= 10^4 sampled outputs (one in every (block,
+    col-group) cell among them)."""
+    base = _MB[li]
+    print(f"mobilenet-v2 nhwc layer {base.name}", flush=True)
+    w, x = workloads.gen_layer(base, 128)
+    xh = x.permute(0, 2, 3, 1).contiguous().cuda()
+    x64 = x.double().numpy()
+    for N in (16, 32):
+        packed = onexn.prepare_layer(w, N, 0.5, False)
+        y = packed.forward(xh, 1, 0, "nhwc").permute(0, 3, 1, 2).contiguous()
+        torch.cuda.synchronize()
+        pr = oracle.prune(w.double().numpy(), N, 0.5, False)
+        assert packed.t == pr.t
+        idx = sample_indices(tuple(y.shape), 10000, li * 37 + N, N)
+        got = y.reshape(-1)[torch.from_numpy(idx).cuda()].double().cpu().numpy()
+        ref = oracle.conv2d_at(x64, pr.wbar, idx)
+        assert rel_err(got, ref) <= 1e-5, (base.name, N)
+
+
+def test_config1_full_size_sampled_nhwc():
+    wl = workloads.config1()
+    layer = wl.layers[0]
+    w, x = workloads.gen_layer(layer, wl.batch)
+    packed = onexn.prepare_layer(w, layer.N, layer.p, layer.rearrange)
+    y = packed.forward(x.permute(0, 2, 3, 1).contiguous().cuda(), 1, 0, "nhwc").permute(0, 3, 1, 2).contiguous()
+    torch.cuda.synchronize()
+    pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+    _check_sampled(layer, wl.batch, "f32", "f32", y, pr, x)
+
+
 @pytest.mark.parametrize("wgs", ["1", "5", "default"])
 @pytest.mark.parametrize("hw", [(12, 12), (7, 7)], ids=["hw%4=0", "hw%4!=0"])
 @pytest.mark.parametrize("N,groups,m", [
