@@ -224,7 +224,13 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
  *   dD[z][i][q][r] = sum_{b,oh,ow} dY[b][gN+i][oh][ow] * X[b][I[z]][oh*sh-ph+q][ow*sw-pw+r],
  *   fp32 [t][N][kh][kw] (rows gN+i >= n get 0); x_dev [batch][m][H][W] and
  *   dy_dev in xdt (F32 or BF16).
- * Both accumulate in fp32 in a fixed order (results do not vary run to run).
+ * Both accumulate in fp32.  The input gradient, and the weight gradient of
+ * every layer except those below, sum in a fixed order (results do not vary
+ * run to run).  For 1x1 stride-1 fp32 layers at N = 16 or 32 with few tiles
+ * of kept blocks (fewer than four workgroups per CU), the weight gradient
+ * splits the pixels over workgroups and adds their sums with atomics into the
+ * zeroed dD, so the last bits can vary run to run; setting the tuning
+ * "bwd_split" to 1 makes it one range per tile (fixed order, slower).
  * Arguments, ownership, the int32 size limits and the errors are those of
  * onexn_conv2d_fwd; P, I, D are the forward's BSR arrays.
  */
@@ -274,7 +280,7 @@ onexn_status onexn_fc_fwd(const int32_t* P_dev, const int32_t* I_dev, const void
  *   "pwb_kernel"  1x1 bf16 N = 32: 1 register-gathered, 2 LDS-staged
  *   "pw_wgs", "pwb_gp", "pwb_rp", "pwb_wgs", "direct_kdb", "direct_tile",
  *   "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "kxkf_split",
- *   "nhwc_tile":
+ *   "nhwc_tile", "bwd_kernel", "bwd_split":
  *                 tile shapes, workgroup counts and pipeline depths of the
  *                 kernel families (a value the family cannot use falls back to
  *                 its default, or makes the conv call fail with UNSUPPORTED).

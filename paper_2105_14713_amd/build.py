@@ -22,7 +22,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 HIP_SOURCES = ["onexn_conv.hip", "conv_generic.hip", "conv_pw_tile.hip", "conv_pw_bf16r.hip",
                "conv_pw_bf16s.hip", "conv_kxk.hip", "conv_kxk_fma.hip", "conv_pw_fma.hip", "conv_pw_direct.hip",
                "conv_pw_nhwc.hip",
-               "mask_dev.hip", "conv_bwd.hip"]
+               "mask_dev.hip", "conv_bwd.hip", "conv_bwd_pw.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I" + INC, "-I" + CSRC]
 
 

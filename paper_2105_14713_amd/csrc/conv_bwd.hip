@@ -26,6 +26,7 @@
 // kernels accumulate in fp32 and their results do not depend on timing.
 
 #include "conv_common.h"
+#include "onexn_internal.h"
 
 namespace onexn {
 namespace {
@@ -273,6 +274,9 @@ extern "C" onexn_status onexn_conv2d_bwd_data(const int32_t* P_dev, const int32_
     a.I = I_dev;
     a.D = D_dev;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // 1x1 stride-1 fp32 layers at N = 16 / 32: the matrix-core kernel.
+    if (bwd_data_pw_applies(a, wdt, dxdt, batch) && tuning(kTuneBwdKernel) != 1)
+        return launch_bwd_data_pw(a, dy_dev, dx_dev, s);
     if (wdt == ONEXN_F32) return launch_bwd_data<float, float>(a, batch, dy_dev, dx_dev, s);
     if (dxdt == ONEXN_BF16) return launch_bwd_data<uint16_t, uint16_t>(a, batch, dy_dev, dx_dev, s);
     return launch_bwd_data<uint16_t, float>(a, batch, dy_dev, dx_dev, s);
@@ -295,6 +299,9 @@ extern "C" onexn_status onexn_conv2d_bwd_weight(const int32_t* P_dev, const int3
     if (t == 0) return ONEXN_OK;
     a.I = I_dev;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // 1x1 stride-1 fp32 layers at N = 16 / 32: the matrix-core kernel.
+    if (bwd_weight_pw_applies(a, xdt, batch) && tuning(kTuneBwdKernel) != 1)
+        return launch_bwd_weight_pw(a, x_dev, dy_dev, dD_dev, s);
     if (xdt == ONEXN_F32) return launch_bwd_weight<float>(a, x_dev, dy_dev, dD_dev, s);
     return launch_bwd_weight<uint16_t>(a, x_dev, dy_dev, dD_dev, s);
 }

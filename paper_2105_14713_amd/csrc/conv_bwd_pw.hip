@@ -1,0 +1,464 @@
+// Input gradient of a 1x1 (stride 1, no padding) 1xN-pruned convolution on
+// matrix cores: fp32, NCHW, N in {16, 32}.
+//
+// Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
+// (arXiv 2105.14713), Sec. 3.4 (Eq. 7 with Omega-bar, stored as Eq. 8's BSR)
+// and Sec. 4.1 (fine-tuning with the pattern fixed).  For a 1x1 layer the
+// adjoint of Eq. 7 is
+//     dX[c][pixel] = sum_g sum_{i < N} Wt_g[c][i] * dY[gN + i][pixel],
+//     Wt_g[c][i] = D[z][i] if col-group g keeps input channel c at block z,
+//                  else 0,
+// a dense contraction over the output channels with Omega-bar's transpose
+// as the left operand.
+//
+// Work.  A workgroup of eight waves computes 32 input channels x 256 pixels
+// (each wave one 32-pixel column block) with v_mfma_f32_32x32x2f32: row =
+// input channel, column = pixel, one col-group (N output channels, N / 2
+// steps) after another.  Col-groups that keep none of the 32 channels are
+// skipped.
+//  - Index.  I ascends within a col-group, so the blocks of a col-group whose
+//    channel falls in [c0, c0 + 32) are one run.  In a prologue each thread
+//    finds one col-group's run by narrowing with 32 samples at a time (one
+//    round of independent loads per 32x narrowing), then records the run's
+//    block per channel in LDS.
+//  - A.  The 32 x N tile Wt_g is built in LDS (double-buffered, one
+//    col-group ahead; rows are the runs' D rows, zero where a channel is not
+//    kept) and read one float per lane and step.
+//  - B.  dY rows gN .. gN+N-1 at the wave's pixels, loaded into registers
+//    one col-group ahead.
+// Every output element is written once, by one lane, after a fixed-order
+// accumulation: the result does not depend on timing.
+
+#include "lds_copy.h"
+#include "pw_common.h"
+
+namespace onexn {
+namespace {
+
+constexpr int kBpWaves = 8;
+constexpr int kBpThreads = 64 * kBpWaves;
+constexpr int kBpNB = 1;                                // 32-pixel column blocks per wave
+constexpr int kBpPix = kBpWaves * kBpNB * 32;           // pixels per workgroup
+constexpr int kBpMaxG = 256;                            // col-groups (one prologue thread each)
+
+template <int N>
+__global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_pw(ConvArgs a, const float* __restrict__ dy,
+                                                           float* __restrict__ dx) {
+    typedef PwMfma<32> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int S = N / 2;                            // MFMA steps per col-group
+    constexpr int AP = N + 1;                           // LDS pitch of a Wt row (floats)
+    __shared__ int32_t sZ[kBpMaxG][32];                 // block of (g, channel), or -1
+    __shared__ int32_t sGl[kBpMaxG];                    // col-groups with a kept block in the tile
+    __shared__ int32_t sCnt[kBpWaves];
+    __shared__ float sA[2][32 * AP];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t c0 = int32_t(blockIdx.y) * 32;
+    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;
+
+    // ---- Index prologue: thread g < G finds the run of col-group g.  (I through
+    // a range-checked buffer: one 32-bit offset register per load.)
+    const int32_t g = tid;
+    bool any = false;
+    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(a.t * 4), kRawBufferFlags);
+    auto ld_i = [&](int32_t e) { return int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)); };
+    if (g < a.G) {
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        // Narrow [lo, hi) to the first entry with I >= c0 (entries before lo
+        // are < c0, I[hi] >= c0 or hi = ze).
+        int32_t lo = zb, hi = ze;
+        while (hi - lo > 32) {
+            const int32_t step = (hi - lo + 31) / 32;
+            int32_t below = 0;   // samples k (I[lo + k*step] < c0) form a prefix
+#pragma unroll
+            for (int k = 0; k < 32; ++k) {
+                const int32_t e = lo + k * step;
+                below += (e < hi && ld_i(e) < c0) ? 1 : 0;
+            }
+            const int32_t nlo = below == 0 ? lo : lo + (below - 1) * step + 1;
+            hi = below == 0 ? lo : min(hi, lo + below * step);
+            lo = nlo;
+        }
+        int32_t below = 0;   // the entries [lo, hi): those below c0
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = lo + k;
+            below += (e < hi && ld_i(e) < c0) ? 1 : 0;
+        }
+        const int32_t first = lo + below;
+        // The run: up to 32 entries from first whose channel is below c0 + 32.
+#pragma unroll
+        for (int k = 0; k < 32; ++k) sZ[g][k] = -1;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = first + k;
+            const int32_t c = e < ze ? ld_i(e) : INT32_MAX;
+            if (c >= c0 && c < c0 + 32 && c < a.m) {
+                sZ[g][c - c0] = e;
+                any = true;
+            }
+        }
+    }
+    // Compact the col-groups with a kept block, in order.
+    const uint64_t bal = __ballot(any);
+    if (lane == 0) sCnt[wave] = __builtin_popcountll(bal);
+    __syncthreads();
+    int32_t base = 0, ng = 0;
+#pragma unroll
+    for (int w = 0; w < kBpWaves; ++w) {
+        base += w < wave ? sCnt[w] : 0;
+        ng += sCnt[w];
+    }
+    if (any) sGl[base + __builtin_popcountll(bal & ((uint64_t(1) << lane) - 1))] = g;
+    __syncthreads();
+
+    // ---- Lane roles.  A: row (input channel c0 + lane % 32), entry parity
+    // kk.  B: pixel column lane % 32 of each block, output channel 2s + kk.
+    const int col = lane & 31, kk = lane >> 5;
+    const int32_t HWo = a.HWo;
+    const int32_t ybytes = int32_t(int64_t(a.npix / HWo) * a.n * HWo * 4);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(ybytes), kRawBufferFlags);
+    uint32_t yo[kBpNB];   // byte offset of the pixel's dY value at output channel 0 (or out of range)
+    int64_t xo[kBpNB];    // element offset of its dX value at channel 0 (or -1)
+#pragma unroll
+    for (int nb = 0; nb < kBpNB; ++nb) {
+        const int32_t p = p0 + (wave * kBpNB + nb) * 32 + col;
+        yo[nb] = kBufferOutOfRange;
+        xo[nb] = -1;
+        if (p < a.npix) {
+            const int32_t b = p / HWo, hw = p - b * HWo;
+            yo[nb] = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
+            xo[nb] = int64_t(b) * a.m * HWo + hw;
+        }
+    }
+    const uint32_t chb = uint32_t(HWo) * 4;   // bytes between dY channels
+    // The lane's part of the offset in the vector offset (range-checked: a
+    // pixel past the last image reads zeros), the step's output channel pair
+    // in the scalar offset; in a ragged last col-group a row past n takes an
+    // out-of-range vector offset instead.
+    uint32_t yk[kBpNB];
+#pragma unroll
+    for (int nb = 0; nb < kBpNB; ++nb) yk[nb] = yo[nb] + uint32_t(kk) * chb;
+    auto load_b = [&](float (&bv)[S][kBpNB], int32_t gg) __attribute__((always_inline)) {
+        const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
+        if (ob + N <= a.n) {
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+#pragma unroll
+                for (int nb = 0; nb < kBpNB; ++nb)
+                    bv[s][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        rY, int32_t(yk[nb]), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        } else {
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+#pragma unroll
+                for (int nb = 0; nb < kBpNB; ++nb) {
+                    const bool ok = ob + 2 * s + kk < a.n;
+                    bv[s][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        rY, int32_t(ok ? yk[nb] + uint32_t(ob + 2 * s) * chb : kBufferOutOfRange), 0, 0));
+                }
+        }
+    };
+    // The Wt tile of col-group gg: thread t holds elements t, t + 256, ...
+    // of the 32 x N tile (row-major), fetched before the current col-group's
+    // multiplies and written after them.
+    constexpr int AE = 32 * N / kBpThreads;   // tile elements per thread
+    const float* __restrict__ D = static_cast<const float*>(a.D);
+    auto fetch_a = [&](float (&av)[AE], int32_t gg) __attribute__((always_inline)) {
+#pragma unroll
+        for (int k = 0; k < AE; ++k) {
+            const int32_t e = tid + k * kBpThreads, r = e / N, i = e - r * N;
+            const int32_t z = sZ[gg][r];
+            av[k] = z >= 0 ? D[int64_t(z) * N + i] : 0.f;
+        }
+    };
+    auto put_a = [&](const float (&av)[AE], int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int k = 0; k < AE; ++k) {
+            const int32_t e = tid + k * kBpThreads, r = e / N, i = e - r * N;
+            sA[buf][r * AP + i] = av[k];
+        }
+    };
+
+    acc_t acc[kBpNB];
+#pragma unroll
+    for (int nb = 0; nb < kBpNB; ++nb)
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) acc[nb][r] = 0.f;
+
+    auto multiply = [&](int buf, const float (&bv)[S][kBpNB]) __attribute__((always_inline)) {
+        const float* ar = &sA[buf][col * AP + kk];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const float av = ar[2 * s];
+#pragma unroll
+            for (int nb = 0; nb < kBpNB; ++nb) acc[nb] = M::step(av, bv[s][nb], acc[nb]);
+        }
+    };
+
+    if (ng > 0) {
+        float b0[S][kBpNB], b1[S][kBpNB], af[AE];
+        fetch_a(af, sGl[0]);
+        load_b(b0, sGl[0]);
+        put_a(af, 0);
+        __syncthreads();
+        // Col-group j is multiplied from LDS buffer j % 2 and register set
+        // j % 2; col-group j + 1's operands are fetched first.
+        for (int32_t j = 0; j < ng; j += 2) {
+            if (j + 1 < ng) {
+                fetch_a(af, sGl[j + 1]);
+                load_b(b1, sGl[j + 1]);
+            }
+            multiply(0, b0);
+            if (j + 1 >= ng) break;
+            put_a(af, 1);
+            __syncthreads();
+            if (j + 2 < ng) {
+                fetch_a(af, sGl[j + 2]);
+                load_b(b0, sGl[j + 2]);
+            }
+            multiply(1, b1);
+            if (j + 2 < ng) put_a(af, 0);
+            __syncthreads();
+        }
+    }
+
+    // ---- Store: MFMA (row, col) of block nb -> dX channel c0 + row, the
+    // block's pixel col.
+#pragma unroll
+    for (int nb = 0; nb < kBpNB; ++nb) {
+        if (xo[nb] < 0) continue;
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) {
+            const int32_t c = c0 + M::row(lane, r);
+            if (c < a.m) store_out(&dx[xo[nb] + int64_t(c) * HWo], acc[nb][r]);
+        }
+    }
+}
+
+}  // namespace
+
+bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
+    if (wdt != ONEXN_F32 || dxdt != ONEXN_F32) return false;
+    if (a.N != 16 && a.N != 32) return false;
+    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
+    if (a.G > kBpMaxG) return false;
+    if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31)) return false;   // 32-bit buffer offsets
+    return true;
+}
+
+onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hipStream_t s) {
+    const int64_t ptiles = (int64_t(a.npix) + kBpPix - 1) / kBpPix;
+    const int64_t ctiles = (int64_t(a.m) + 31) / 32;
+    if (ptiles > INT32_MAX || ctiles > 65535)
+        return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_data: grid out of range");
+    const dim3 grid{uint32_t(ptiles), uint32_t(ctiles), 1};
+    if (a.N == 32)
+        hipLaunchKernelGGL(bwd_data_pw<32>, grid, dim3(kBpThreads), 0, s, a, static_cast<const float*>(dy),
+                           static_cast<float*>(dx));
+    else
+        hipLaunchKernelGGL(bwd_data_pw<16>, grid, dim3(kBpThreads), 0, s, a, static_cast<const float*>(dy),
+                           static_cast<float*>(dx));
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_data: launch failed: %s", hipGetErrorString(err));
+    return ONEXN_OK;
+}
+
+}  // namespace onexn
+
+// ---------------------------------------------------------------------------
+// Weight gradient of the kept blocks of a 1x1 (stride 1, no padding) layer on
+// matrix cores: fp32, NCHW, N in {16, 32}.
+//
+//     dD[z][i] = sum over pixels of X[I[z]][pixel] * dY[gN + i][pixel]
+//
+// (Sec. 3.4's BSR layout, z a kept block of col-group g).  For a tile of N
+// consecutive kept blocks of one col-group this is an N x N contraction over
+// the pixels: rows = blocks, columns = block rows i, with
+// v_mfma_f32_32x32x2f32 (N = 32) or v_mfma_f32_16x16x4f32 (N = 16).  A
+// workgroup of four waves stages 128-pixel chunks of the tile's N gathered
+// input rows and the col-group's N dY rows in LDS (coalesced along pixels,
+// each thread one pixel; the next chunk's values are loaded into registers
+// while this chunk is multiplied); each wave multiplies 32 of the chunk's
+// pixels, and the four partial sums are added through LDS in wave order at
+// the end.  Layers with few tiles split their pixels over several
+// workgroups, whose sums are added into dD (zeroed first) with atomic adds:
+// those layers' results can differ in the last bits from run to run; with
+// one range per tile (the default where tiles suffice) every element is
+// stored once after a fixed-order accumulation.
+// ---------------------------------------------------------------------------
+
+namespace onexn {
+namespace {
+
+constexpr int kBwWaves = 4;
+constexpr int kBwThreads = 64 * kBwWaves;
+constexpr int kBwCh = 128;                     // pixels per staged chunk (one per thread and row pair)
+constexpr int kBwPitch = kBwCh + 1;            // LDS row pitch (floats)
+
+__global__ void __launch_bounds__(256) bw_zero(float* __restrict__ p, int64_t n) {
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) p[i] = 0.f;
+}
+
+template <int N>
+__global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const float* __restrict__ x,
+                                                             const float* __restrict__ dy,
+                                                             float* __restrict__ dD, int32_t tiles_per_g,
+                                                             int32_t nsplit) {
+    typedef PwMfma<N> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int KS = M::KS;                  // pixels per MFMA step
+    constexpr int RPT = N * kBwCh / kBwThreads;   // rows per thread and operand (one pixel each)
+    static_assert(kBwThreads % kBwCh == 0, "a thread keeps one pixel of every chunk");
+    __shared__ float sX[N * kBwPitch];
+    __shared__ float sY[N * kBwPitch];
+    __shared__ float sR[kBwWaves][64 * M::ACC];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // Work item: (col-group, tile of N kept blocks, pixel range).
+    const int32_t item = blockIdx.x;
+    const int32_t split = item % nsplit;
+    const int32_t gt = item / nsplit;
+    const int32_t g = gt / tiles_per_g, tile = gt - g * tiles_per_g;
+    int32_t zb, ze;
+    group_range(a, g, zb, ze);
+    const int32_t e0 = zb + tile * N;
+    if (e0 >= ze) return;                      // (uniform: the col-group has fewer tiles)
+    const int32_t pb = int32_t(int64_t(a.npix) * split / nsplit);
+    const int32_t pe = int32_t(int64_t(a.npix) * (split + 1) / nsplit);
+
+    // This thread's pixel of each chunk and its rows (r0 + 2 j for N = 32, ...).
+    const int px = tid % kBwCh, r0 = tid / kBwCh;
+    constexpr int RS = kBwThreads / kBwCh;     // row stride between a thread's rows
+    const int32_t HWo = a.HWo;
+    const int32_t batch = a.npix / HWo;
+    const uint32_t chb = uint32_t(HWo) * 4;
+    const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HWo * 4)),
+        kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
+        kRawBufferFlags);
+    // Row offsets (bytes, pixel part excluded): the tile's blocks' input
+    // channels and the col-group's output channels; a block past the
+    // col-group, a channel outside [0, m) or a row past n reads zeros.
+    uint32_t xr[RPT], yr[RPT];
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+        const int32_t r = r0 + RS * j;
+        const int32_t e = e0 + r;
+        const int32_t c = e < ze ? a.I[e] : -1;
+        xr[j] = uint32_t(c) < uint32_t(a.m) ? uint32_t(c) * chb : kBufferOutOfRange;
+        const int32_t o = g * N + r;
+        yr[j] = o < a.n ? uint32_t(o) * chb : kBufferOutOfRange;
+    }
+    float vx[RPT], vy[RPT];
+    auto load = [&](int32_t p0) __attribute__((always_inline)) {
+        const int32_t p = p0 + px;
+        uint32_t bx = kBufferOutOfRange, by = kBufferOutOfRange;
+        if (p < pe) {
+            const int32_t b = p / HWo, hw = p - b * HWo;
+            bx = uint32_t((int64_t(b) * a.m * HWo + hw) * 4);
+            by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
+        }
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rX, int32_t(bx + xr[j]), 0, 0));
+            vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
+        }
+    };
+    auto put = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            sX[(r0 + RS * j) * kBwPitch + px] = vx[j];
+            sY[(r0 + RS * j) * kBwPitch + px] = vy[j];
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    // Lane roles: A (block row lane % N, pixel k = lane / N of a step), B
+    // (column lane % N, same k).
+    const int rc = lane % N, k = lane / N;
+    const float* ax = sX + rc * kBwPitch + wave * 32 + k;
+    const float* by = sY + rc * kBwPitch + wave * 32 + k;
+
+    if (pb < pe) {
+        load(pb);
+        for (int32_t p0 = pb; p0 < pe; p0 += kBwCh) {
+            __syncthreads();   // the previous chunk's reads are done
+            put();
+            __syncthreads();
+            if (p0 + kBwCh < pe) load(p0 + kBwCh);
+#pragma unroll
+            for (int st = 0; st < 32 / KS; ++st) acc = M::step(ax[st * KS], by[st * KS], acc);
+        }
+    }
+
+    // The four waves' partial sums, added in wave order by wave 0.
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) sR[wave][r * 64 + lane] = acc[r];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r)
+        acc[r] = ((sR[0][r * 64 + lane] + sR[1][r * 64 + lane]) + sR[2][r * 64 + lane]) + sR[3][r * 64 + lane];
+    // MFMA (row, col): block e0 + row, block row col.
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) {
+        const int32_t e = e0 + M::row(lane, r);
+        if (e >= ze) continue;
+        float* dst = dD + int64_t(e) * N + rc;
+        if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
+        else *dst = acc[r];
+    }
+}
+
+}  // namespace
+
+bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
+    if (xdt != ONEXN_F32) return false;
+    if (a.N != 16 && a.N != 32) return false;
+    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
+    if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31) ||
+        int64_t(batch) * a.m * a.HWo * 4 >= (int64_t(1) << 31))
+        return false;   // 32-bit buffer offsets
+    return true;
+}
+
+onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
+    const int64_t tiles_per_g = (int64_t(a.m) + a.N - 1) / a.N;   // a col-group keeps at most m blocks
+    const int64_t tiles = (int64_t(a.t) + a.N - 1) / a.N + a.G;   // tiles that hold blocks, at most
+    // Pixel ranges per tile: enough workgroups for four per CU, each range
+    // at least 1024 pixels; one range where the tiles suffice (stored, not added).
+    int64_t nsplit = (4 * int64_t(device_cu_count()) + tiles - 1) / tiles;
+    nsplit = std::max<int64_t>(1, std::min<int64_t>(nsplit, a.npix / 1024));
+    if (tuning(kTuneBwdSplit) >= 1) nsplit = tuning(kTuneBwdSplit);
+    const int64_t grid = int64_t(a.G) * tiles_per_g * nsplit;
+    if (grid < 1 || grid > INT32_MAX)
+        return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_weight: grid out of range");
+    if (nsplit > 1) {
+        const int64_t n = int64_t(a.t) * a.N;
+        hipLaunchKernelGGL(bw_zero, dim3(uint32_t(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256), 0, s, dD, n);
+    }
+    if (a.N == 32)
+        hipLaunchKernelGGL(bwd_weight_pw<32>, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a,
+                           static_cast<const float*>(x), static_cast<const float*>(dy), dD, int32_t(tiles_per_g),
+                           int32_t(nsplit));
+    else
+        hipLaunchKernelGGL(bwd_weight_pw<16>, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a,
+                           static_cast<const float*>(x), static_cast<const float*>(dy), dD, int32_t(tiles_per_g),
+                           int32_t(nsplit));
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(err));
+    return ONEXN_OK;
+}
+
+}  // namespace onexn

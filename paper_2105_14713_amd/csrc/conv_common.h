@@ -214,6 +214,10 @@ onexn_status launch_pw_direct(ConvArgs a, hipStream_t stream);
 onexn_status launch_pw_fma(ConvArgs a, hipStream_t stream);
 bool kxk_fma_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
 bool pw_nhwc_applies(const ConvArgs& a, onexn_dtype xdt, onexn_dtype ydt, onexn_layout layout);
+bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch);
+onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hipStream_t stream);
+bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch);
+onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t stream);
 onexn_status launch_pw_nhwc(ConvArgs a, hipStream_t stream);
 onexn_status launch_kxk_fma(ConvArgs a, hipStream_t stream);
 onexn_status launch_kxk(ConvArgs a, hipStream_t stream);

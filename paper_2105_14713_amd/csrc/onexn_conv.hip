@@ -28,7 +28,7 @@ std::atomic<int32_t> g_tuning[kTuneCount];
 const char* const kTuneNames[kTuneCount] = {
     "kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile", "fma_tpw",
     "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs", "kxkf_split",
-    "nhwc_tile"};
+    "nhwc_tile", "bwd_kernel", "bwd_split"};
 
 }  // namespace
 

@@ -35,6 +35,8 @@ enum Tune : int {
     kTunePwbWgs,       // LDS-staged bf16 1x1: workgroups
     kTuneKxfSplit,     // 3x3 FMA (N <= 8): waves per unit (1, 4)
     kTuneNhwcTile,     // NHWC 1x1: column blocks per tile
+    kTuneBwdKernel,    // backward: 1 the general kernels for every layer
+    kTuneBwdSplit,     // 1x1 weight gradient: pixel ranges per tile
     kTuneCount
 };
 constexpr int32_t kTuneAuto = -1;

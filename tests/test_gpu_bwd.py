@@ -45,6 +45,11 @@ CASES = [  # (n, m, k, stride, pad, B, H, W, N)
     (9, 6, 7, 2, 3, 1, 15, 13, 2),
     (7, 20, 5, 3, 2, 2, 13, 12, 1),
     (64, 3, 7, 2, 3, 1, 20, 20, 32),    # stem-like
+    # 1x1 stride 1 at N = 16 / 32: the matrix-core input gradient
+    (80, 45, 1, 1, 0, 3, 7, 9, 32),     # ragged last col-group, pixels not a multiple of 32
+    (40, 70, 1, 1, 0, 2, 10, 10, 16),   # three channel tiles, the last partial
+    (96, 300, 1, 1, 0, 1, 9, 9, 32),    # col-groups of up to 300 blocks (narrowing rounds)
+    (48, 1100, 1, 1, 0, 1, 5, 4, 16),   # col-groups longer than 1024 blocks
 ]
 
 
@@ -104,12 +109,38 @@ def test_bwd_resnet50_layer_shape_and_reproducibility():
     np.testing.assert_array_equal(dD, dD2)
 
 
-def test_bwd_everything_pruned():
-    w, x = workloads.gen_integer_layer(seed=1, cout=32, cin=5, k=3, batch=1, H=6)
-    layer = onexn.prepare_layer(w, 16, 1.0, False)
+@pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "general"])
+@pytest.mark.parametrize("N", [16, 32])
+def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
+    """The 1x1 gradients through the matrix-core kernels (the weight gradient
+    with one pixel range per tile, and with three whose sums are added) and
+    through the general ones (bwd_kernel = 1): fp32 random, 300 -> 256, and
+    integer data exactly."""
+    if kernel == "general":
+        tune("bwd_kernel", 1)
+    if kernel == "matrix_split3":
+        tune("bwd_split", 3)
+    gen = torch.Generator().manual_seed(23 + N)
+    w = workloads.gen_weight(gen, 256, 300, 1)
+    x = workloads.gen_activation(gen, (2, 300, 12, 11))
+    dy = torch.randn((2, 256, 12, 11), generator=gen)
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, 0.5, 1, 0)
+    assert rel_err(dx, ref_dx) <= 1e-5
+    assert rel_err(dD, ref_dD) <= 1e-5
+    wi, xi = workloads.gen_integer_layer(seed=N, cout=72, cin=50, k=1, batch=3, H=9, W=13, wmax=2, xmax=2)
+    dyi = torch.randint(-2, 3, (3, 72, 9, 13), generator=gen).float()
+    dx, dD, ref_dx, ref_dD = _bwd(wi, xi, dyi, N, 0.5, 1, 0)
+    np.testing.assert_array_equal(dx, ref_dx)
+    np.testing.assert_array_equal(dD, ref_dD)
+
+
+@pytest.mark.parametrize("k,N", [(3, 16), (1, 32)])
+def test_bwd_everything_pruned(k, N):
+    w, x = workloads.gen_integer_layer(seed=1, cout=32, cin=5, k=k, batch=1, H=6)
+    layer = onexn.prepare_layer(w, N, 1.0, False)
     dy = torch.ones((1, 32, 6, 6), device="cuda")
-    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, 32, 5, dy, (6, 6), 1, 1)
-    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, 32, 16, (3, 3), x.cuda(), dy, 1, 1)
+    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, 32, 5, dy, (6, 6), 1, k // 2)
+    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, 32, N, (k, k), x.cuda(), dy, 1, k // 2)
     torch.cuda.synchronize()
     assert layer.t == 0 and dD.numel() == 0
     assert torch.all(dx == 0)

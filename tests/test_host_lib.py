@@ -247,7 +247,7 @@ def test_set_tuning_errors(lib):
     assert lib.onexn_set_tuning(b"kxk_split", -2) == 2
     for name in ("kernel", "pw_kernel", "pw_wgs", "pwb_gp", "pwb_rp", "direct_kdb", "direct_tile",
                  "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "pwb_kernel", "pwb_wgs",
-                 "kxkf_split", "nhwc_tile"):
+                 "kxkf_split", "nhwc_tile", "bwd_kernel", "bwd_split"):
         assert lib.onexn_set_tuning(name.encode(), -1) == 0, name
 
 
