@@ -230,7 +230,9 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
  * of kept blocks (fewer than four workgroups per CU), the weight gradient
  * splits the pixels over workgroups and adds their sums with atomics into the
  * zeroed dD, so the last bits can vary run to run; setting the tuning
- * "bwd_split" to 1 makes it one range per tile (fixed order, slower).
+ * "bwd_split" to 1 makes it one range per tile (fixed order, slower).  Such
+ * a call launches a fill of dD first: a HIP error from its second launch may
+ * leave dD zeroed.
  * Arguments, ownership, the int32 size limits and the errors are those of
  * onexn_conv2d_fwd; P, I, D are the forward's BSR arrays.
  */

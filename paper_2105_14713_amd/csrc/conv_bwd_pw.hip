@@ -447,6 +447,9 @@ onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* 
     if (nsplit > 1) {
         const int64_t n = int64_t(a.t) * a.N;
         hipLaunchKernelGGL(bw_zero, dim3(uint32_t(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256), 0, s, dD, n);
+        const hipError_t zerr = hipGetLastError();
+        if (zerr != hipSuccess)
+            return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(zerr));
     }
     if (a.N == 32)
         hipLaunchKernelGGL(bwd_weight_pw<32>, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a,
