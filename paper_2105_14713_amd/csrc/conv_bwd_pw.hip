@@ -272,24 +272,26 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
 }  // namespace onexn
 
 // ---------------------------------------------------------------------------
-// Weight gradient of the kept blocks of a 1x1 (stride 1, no padding) layer on
-// matrix cores: fp32, NCHW, N in {16, 32}.
+// Weight gradient of the kept blocks on matrix cores: fp32, NCHW, N in
+// {16, 32}, any kernel size, stride and padding.
 //
-//     dD[z][i] = sum over pixels of X[I[z]][pixel] * dY[gN + i][pixel]
+//     dD[z][i][q][r] = sum over output pixels of
+//                      X[I[z]][oh*sh - ph + q][ow*sw - pw + r] * dY[gN + i][oh][ow]
 //
 // (Sec. 3.4's BSR layout, z a kept block of col-group g).  For a tile of N
-// consecutive kept blocks of one col-group this is an N x N contraction over
-// the pixels: rows = blocks, columns = block rows i, with
-// v_mfma_f32_32x32x2f32 (N = 32) or v_mfma_f32_16x16x4f32 (N = 16).  A
-// workgroup of four waves stages 128-pixel chunks of the tile's N gathered
-// input rows and the col-group's N dY rows in LDS (coalesced along pixels,
-// each thread one pixel; the next chunk's values are loaded into registers
-// while this chunk is multiplied); each wave multiplies 32 of the chunk's
-// pixels, and the four partial sums are added through LDS in wave order at
-// the end.  Layers with few tiles split their pixels over several
+// consecutive kept blocks of one col-group and one tap (q, r) this is an
+// N x N contraction over the output pixels: rows = blocks, columns = block
+// rows i, with v_mfma_f32_32x32x2f32 (N = 32) or v_mfma_f32_16x16x4f32
+// (N = 16).  A workgroup of four waves stages 128-pixel chunks of the tile's
+// N gathered input rows (at the tap's shifted positions, zero in the padding)
+// and the col-group's N dY rows in LDS (coalesced along pixels, each thread
+// one pixel; the next chunk's values are loaded into registers while this
+// chunk is multiplied); each wave multiplies 32 of the chunk's pixels, and
+// the four partial sums are added through LDS in wave order at the end.
+// Layers with few (tile, tap) items split their pixels over several
 // workgroups, whose sums are added into dD (zeroed first) with atomic adds:
 // those layers' results can differ in the last bits from run to run; with
-// one range per tile (the default where tiles suffice) every element is
+// one range per item (the default where items suffice) every element is
 // stored once after a fixed-order accumulation.
 // ---------------------------------------------------------------------------
 
@@ -321,10 +323,12 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // Work item: (col-group, tile of N kept blocks, pixel range).
+    // Work item: (col-group, tile of N kept blocks, tap, pixel range).
     const int32_t item = blockIdx.x;
     const int32_t split = item % nsplit;
-    const int32_t gt = item / nsplit;
+    const int32_t tap = (item / nsplit) % a.KK;            // kernel tap (q, r) of the work item
+    const int32_t gt = item / nsplit / a.KK;
+    const int32_t q = tap / a.kw, r = tap - q * a.kw;
     const int32_t g = gt / tiles_per_g, tile = gt - g * tiles_per_g;
     int32_t zb, ze;
     group_range(a, g, zb, ze);
@@ -336,11 +340,11 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
     // This thread's pixel of each chunk and its rows (r0 + 2 j for N = 32, ...).
     const int px = tid % kBwCh, r0 = tid / kBwCh;
     constexpr int RS = kBwThreads / kBwCh;     // row stride between a thread's rows
-    const int32_t HWo = a.HWo;
+    const int32_t HWo = a.HWo, HW = a.H * a.W;
     const int32_t batch = a.npix / HWo;
-    const uint32_t chb = uint32_t(HWo) * 4;
+    const uint32_t chb = uint32_t(HWo) * 4, xchb = uint32_t(HW) * 4;   // channel strides of dY and X
     const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HWo * 4)),
+        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HW * 4)),
         kRawBufferFlags);
     const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
@@ -354,7 +358,7 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
         const int32_t r = r0 + RS * j;
         const int32_t e = e0 + r;
         const int32_t c = e < ze ? a.I[e] : -1;
-        xr[j] = uint32_t(c) < uint32_t(a.m) ? uint32_t(c) * chb : kBufferOutOfRange;
+        xr[j] = uint32_t(c) < uint32_t(a.m) ? uint32_t(c) * xchb : kBufferOutOfRange;
         const int32_t o = g * N + r;
         yr[j] = o < a.n ? uint32_t(o) * chb : kBufferOutOfRange;
     }
@@ -363,8 +367,13 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
         const int32_t p = p0 + px;
         uint32_t bx = kBufferOutOfRange, by = kBufferOutOfRange;
         if (p < pe) {
+            // Output pixel p; its input pixel under tap (q, r) (outside the
+            // image: zero padding, read as zeros).
             const int32_t b = p / HWo, hw = p - b * HWo;
-            bx = uint32_t((int64_t(b) * a.m * HWo + hw) * 4);
+            const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+            const int32_t ih = oh * a.sh - a.ph + q, iw = ow * a.sw - a.pw + r;
+            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                bx = uint32_t((int64_t(b) * a.m * HW + int64_t(ih) * a.W + iw) * 4);
             by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
         }
 #pragma unroll
@@ -415,7 +424,7 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
     for (int r = 0; r < M::ACC; ++r) {
         const int32_t e = e0 + M::row(lane, r);
         if (e >= ze) continue;
-        float* dst = dD + int64_t(e) * N + rc;
+        float* dst = dD + (int64_t(e) * N + rc) * a.KK + tap;
         if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
         else *dst = acc[r];
     }
@@ -426,26 +435,25 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
 bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
     if (xdt != ONEXN_F32) return false;
     if (a.N != 16 && a.N != 32) return false;
-    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
     if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31) ||
-        int64_t(batch) * a.m * a.HWo * 4 >= (int64_t(1) << 31))
+        int64_t(batch) * a.m * a.H * a.W * 4 >= (int64_t(1) << 31))
         return false;   // 32-bit buffer offsets
     return true;
 }
 
 onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
     const int64_t tiles_per_g = (int64_t(a.m) + a.N - 1) / a.N;   // a col-group keeps at most m blocks
-    const int64_t tiles = (int64_t(a.t) + a.N - 1) / a.N + a.G;   // tiles that hold blocks, at most
+    const int64_t tiles = ((int64_t(a.t) + a.N - 1) / a.N + a.G) * a.KK;   // (tile, tap) items with blocks, at most
     // Pixel ranges per tile: enough workgroups for four per CU, each range
     // at least 1024 pixels; one range where the tiles suffice (stored, not added).
     int64_t nsplit = (4 * int64_t(device_cu_count()) + tiles - 1) / tiles;
     nsplit = std::max<int64_t>(1, std::min<int64_t>(nsplit, a.npix / 1024));
     if (tuning(kTuneBwdSplit) >= 1) nsplit = tuning(kTuneBwdSplit);
-    const int64_t grid = int64_t(a.G) * tiles_per_g * nsplit;
+    const int64_t grid = int64_t(a.G) * tiles_per_g * a.KK * nsplit;
     if (grid < 1 || grid > INT32_MAX)
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_weight: grid out of range");
     if (nsplit > 1) {
-        const int64_t n = int64_t(a.t) * a.N;
+        const int64_t n = int64_t(a.t) * a.N * a.KK;
         hipLaunchKernelGGL(bw_zero, dim3(uint32_t(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256), 0, s, dD, n);
         const hipError_t zerr = hipGetLastError();
         if (zerr != hipSuccess)
