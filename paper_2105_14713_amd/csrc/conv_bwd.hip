@@ -20,12 +20,24 @@
 // the output pixel whose window puts that tap on it (when the stride
 // divides), weights being wave-uniform loads.
 //
+// bwd_data_fewc.  Layers with at most four input channels (a network's first
+// convolution), fp32: every input channel of a pixel in one lane.  The
+// layer's weights (Omega-bar, dense, [tap][output channel][input channel],
+// zero where pruned) are scattered into LDS once per workgroup.  A wave takes
+// 64 input pixels of one row whose columns share their residue modulo the
+// stride (iw = cb + sw * (64k + lane)), so the taps whose stride divides are
+// the same for the whole wave and the others are skipped; for each such tap
+// and output channel a lane loads one dY value (consecutive lanes,
+// consecutive output columns; out-of-range positions read zeros) and adds it,
+// times the broadcast weights, into its MC channel sums.  Fixed summation
+// order (tap, then output channel).
+//
 // bwd_weight.  A workgroup per (kept block z, tap).  Lanes split the output
 // pixels and keep N partial sums (one per block row) over their pixels, then
 // an LDS tree adds the 256 lanes' sums in a fixed order.  Both
 // kernels accumulate in fp32 and their results do not depend on timing.
 
-#include "conv_common.h"
+#include "lds_copy.h"
 #include "onexn_internal.h"
 
 namespace onexn {
@@ -116,6 +128,88 @@ __global__ void __launch_bounds__(kBwdThreads) bwd_data(ConvArgs a, const TD* __
         }
     }
     dx[(int64_t(b) * a.m + c) * HW + hw] = from_f32<TY>(acc);
+}
+
+constexpr int kFcWaves = 4;
+constexpr int kFcMaxC = 4;                 // input channels bwd_data_fewc takes
+constexpr int kFcMaxLds = 64 * 1024;       // bytes of its weight table
+
+template <int MC>
+__global__ void __launch_bounds__(64 * kFcWaves) bwd_data_fewc(ConvArgs a, const float* __restrict__ dy,
+                                                               float* __restrict__ dx, int32_t cpr,
+                                                               int32_t tasks) {
+    extern __shared__ float sW[];   // [KK][n][MC]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t n = a.n, N = a.N, KK = a.KK;
+    for (int32_t e = tid; e < KK * n * MC; e += 64 * kFcWaves) sW[e] = 0.f;
+    __syncthreads();
+    const float* __restrict__ D = static_cast<const float*>(a.D);
+    for (int32_t g = 0; g < a.G; ++g) {
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        const int32_t per = N * KK;          // floats of a D row
+        for (int32_t e = tid; e < (ze - zb) * per; e += 64 * kFcWaves) {
+            const int32_t zz = e / per, rem = e - zz * per;
+            const int32_t i = rem / KK, tap = rem - i * KK;
+            const int32_t o = g * N + i, c = a.I[zb + zz];
+            if (o < n && c >= 0 && c < MC) sW[(tap * n + o) * MC + c] = D[int64_t(zb + zz) * per + rem];
+        }
+    }
+    __syncthreads();
+
+    const int32_t HWo = a.HWo, HWi = a.H * a.W;
+    const int32_t batch = a.npix / HWo;
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(batch * n * HWo * 4), kRawBufferFlags);
+    const uint32_t chb = uint32_t(HWo) * 4;  // bytes between dY channels
+    const int32_t per_row = a.sw * cpr;      // wave tasks per input row
+    for (int32_t task = int32_t(blockIdx.x) * kFcWaves + wave; task < tasks;
+         task += int32_t(gridDim.x) * kFcWaves) {
+        const int32_t row = task / per_row, rem = task - row * per_row;
+        const int32_t cb = rem / cpr, k = rem - cb * cpr;
+        const int32_t b = row / a.H, ih = row - b * a.H;
+        const int32_t iw = cb + a.sw * (64 * k + lane);
+        const bool in = iw < a.W;
+        const int32_t ybase = b * n * HWo;
+        float acc[MC];
+#pragma unroll
+        for (int c = 0; c < MC; ++c) acc[c] = 0.f;
+        for (int32_t q = 0; q < a.kh; ++q) {
+            const int32_t th = ih + a.ph - q;
+            if (th < 0 || th % a.sh != 0 || th / a.sh >= a.Ho) continue;
+            const int32_t yrow = ybase + (th / a.sh) * a.Wo;
+            for (int32_t r = 0; r < a.kw; ++r) {
+                if (((cb + a.pw - r) % a.sw + a.sw) % a.sw != 0) continue;   // the wave's column residue
+                const int32_t tw = iw + a.pw - r;
+                const bool ok = in && tw >= 0 && tw / a.sw < a.Wo;
+                const int32_t voff = ok ? (yrow + tw / a.sw) * 4 : int32_t(kBufferOutOfRange);
+                const float* w = sW + (q * a.kw + r) * n * MC;
+                int32_t o = 0;
+                for (; o + 8 <= n; o += 8) {
+                    float v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                            rY, voff, int32_t(uint32_t(o + u) * chb), 0));
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+#pragma unroll
+                        for (int c = 0; c < MC; ++c) acc[c] += w[(o + u) * MC + c] * v[u];
+                }
+                for (; o < n; ++o) {
+                    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        rY, voff, int32_t(uint32_t(o) * chb), 0));
+#pragma unroll
+                    for (int c = 0; c < MC; ++c) acc[c] += w[o * MC + c] * v;
+                }
+            }
+        }
+        if (in) {
+#pragma unroll
+            for (int c = 0; c < MC; ++c) dx[(int64_t(b) * a.m + c) * HWi + int64_t(ih) * a.W + iw] = acc[c];
+        }
+    }
 }
 
 template <int N, typename TX>
@@ -232,6 +326,31 @@ onexn_status launch_bwd_data(const ConvArgs& a, int32_t batch, const void* dy, v
     return launched("conv2d_bwd_data");
 }
 
+bool bwd_data_fewc_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
+    return wdt == ONEXN_F32 && dxdt == ONEXN_F32 && a.m <= kFcMaxC &&
+           int64_t(a.KK) * a.n * a.m * 4 <= kFcMaxLds &&
+           int64_t(batch) * a.n * a.HWo * 4 < (int64_t(1) << 31);   // 32-bit buffer offsets
+}
+
+onexn_status launch_bwd_data_fewc(const ConvArgs& a, int32_t batch, const void* dy, void* dx, hipStream_t s) {
+    const int32_t cpr = ((a.W + a.sw - 1) / a.sw + 63) / 64;   // 64-column chunks of a residue class
+    const int64_t tasks = int64_t(batch) * a.H * a.sw * cpr;
+    if (tasks > INT32_MAX) return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_data: grid out of range");
+    const int64_t grid = std::min<int64_t>((tasks + kFcWaves - 1) / kFcWaves, 8 * int64_t(device_cu_count()));
+    const size_t lds = size_t(a.KK) * a.n * a.m * 4;
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(64 * kFcWaves), lds, s, a,
+                           static_cast<const float*>(dy), static_cast<float*>(dx), cpr, int32_t(tasks));
+        return launched("conv2d_bwd_data");
+    };
+    switch (a.m) {
+        case 1: return go(bwd_data_fewc<1>);
+        case 2: return go(bwd_data_fewc<2>);
+        case 3: return go(bwd_data_fewc<3>);
+        default: return go(bwd_data_fewc<4>);
+    }
+}
+
 template <typename TX>
 onexn_status launch_bwd_weight(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
     auto go = [&](auto kern) {
@@ -274,9 +393,13 @@ extern "C" onexn_status onexn_conv2d_bwd_data(const int32_t* P_dev, const int32_
     a.I = I_dev;
     a.D = D_dev;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // 1x1 stride-1 fp32 layers at N = 16 / 32: the matrix-core kernel.
-    if (bwd_data_pw_applies(a, wdt, dxdt, batch) && tuning(kTuneBwdKernel) != 1)
-        return launch_bwd_data_pw(a, dy_dev, dx_dev, s);
+    // fp32 layers with at most four input channels: one lane per input pixel
+    // and all its channels.  fp32 1x1 and 3x3 layers at N = 16 / 32: the
+    // matrix-core kernels.
+    if (tuning(kTuneBwdKernel) != 1) {
+        if (bwd_data_fewc_applies(a, wdt, dxdt, batch)) return launch_bwd_data_fewc(a, batch, dy_dev, dx_dev, s);
+        if (bwd_data_pw_applies(a, wdt, dxdt, batch)) return launch_bwd_data_pw(a, dy_dev, dx_dev, s);
+    }
     if (wdt == ONEXN_F32) return launch_bwd_data<float, float>(a, batch, dy_dev, dx_dev, s);
     if (dxdt == ONEXN_BF16) return launch_bwd_data<uint16_t, uint16_t>(a, batch, dy_dev, dx_dev, s);
     return launch_bwd_data<uint16_t, float>(a, batch, dy_dev, dx_dev, s);

@@ -29,6 +29,8 @@
 // Every output element is written once, by one lane, after a fixed-order
 // accumulation: the result does not depend on timing.
 
+#include <utility>
+
 #include "lds_copy.h"
 #include "pw_common.h"
 
@@ -40,6 +42,35 @@ constexpr int kBpThreads = 64 * kBpWaves;
 constexpr int kBpNB = 1;                                // 32-pixel column blocks per wave
 constexpr int kBpPix = kBpWaves * kBpNB * 32;           // pixels per workgroup
 constexpr int kBpMaxG = 256;                            // col-groups (one prologue thread each)
+
+// First entry in [zb, ze) of a col-group whose input channel is >= c0 (ze if
+// none).  I ascends within a col-group, so the entries below c0 form a
+// prefix; [lo, hi) is narrowed 32 samples at a time (one round of independent
+// loads per 32x narrowing; entries before lo are < c0, and I[hi] >= c0 or
+// hi = ze).
+__device__ __forceinline__ int32_t run_first(__amdgpu_buffer_rsrc_t rI, int32_t zb, int32_t ze, int32_t c0) {
+    auto ld_i = [&](int32_t e) { return int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)); };
+    int32_t lo = zb, hi = ze;
+    while (hi - lo > 32) {
+        const int32_t step = (hi - lo + 31) / 32;
+        int32_t below = 0;   // samples k (I[lo + k*step] < c0) form a prefix
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = lo + k * step;
+            below += (e < hi && ld_i(e) < c0) ? 1 : 0;
+        }
+        const int32_t nlo = below == 0 ? lo : lo + (below - 1) * step + 1;
+        hi = below == 0 ? lo : min(hi, lo + below * step);
+        lo = nlo;
+    }
+    int32_t below = 0;   // the entries [lo, hi): those below c0
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+        const int32_t e = lo + k;
+        below += (e < hi && ld_i(e) < c0) ? 1 : 0;
+    }
+    return lo + below;
+}
 
 template <int N>
 __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_pw(ConvArgs a, const float* __restrict__ dy,
@@ -68,28 +99,7 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     if (g < a.G) {
         int32_t zb, ze;
         group_range(a, g, zb, ze);
-        // Narrow [lo, hi) to the first entry with I >= c0 (entries before lo
-        // are < c0, I[hi] >= c0 or hi = ze).
-        int32_t lo = zb, hi = ze;
-        while (hi - lo > 32) {
-            const int32_t step = (hi - lo + 31) / 32;
-            int32_t below = 0;   // samples k (I[lo + k*step] < c0) form a prefix
-#pragma unroll
-            for (int k = 0; k < 32; ++k) {
-                const int32_t e = lo + k * step;
-                below += (e < hi && ld_i(e) < c0) ? 1 : 0;
-            }
-            const int32_t nlo = below == 0 ? lo : lo + (below - 1) * step + 1;
-            hi = below == 0 ? lo : min(hi, lo + below * step);
-            lo = nlo;
-        }
-        int32_t below = 0;   // the entries [lo, hi): those below c0
-#pragma unroll
-        for (int k = 0; k < 32; ++k) {
-            const int32_t e = lo + k;
-            below += (e < hi && ld_i(e) < c0) ? 1 : 0;
-        }
-        const int32_t first = lo + below;
+        const int32_t first = run_first(rI, zb, ze, c0);
         // The run: up to 32 entries from first whose channel is below c0 + 32.
 #pragma unroll
         for (int k = 0; k < 32; ++k) sZ[g][k] = -1;
@@ -119,21 +129,26 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     // ---- Lane roles.  A: row (input channel c0 + lane % 32), entry parity
     // kk.  B: pixel column lane % 32 of each block, output channel 2s + kk.
     const int col = lane & 31, kk = lane >> 5;
-    const int32_t HWo = a.HWo;
+    const int32_t HWo = a.HWo, HWi = a.H * a.W;
     const int32_t ybytes = int32_t(int64_t(a.npix / HWo) * a.n * HWo * 4);
     const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(ybytes), kRawBufferFlags);
     uint32_t yo[kBpNB];   // byte offset of the pixel's dY value at output channel 0 (or out of range)
     int64_t xo[kBpNB];    // element offset of its dX value at channel 0 (or -1)
+    int32_t ih0[kBpNB], iw0[kBpNB];   // the input position it reads (oh * sh, ow * sw)
 #pragma unroll
     for (int nb = 0; nb < kBpNB; ++nb) {
         const int32_t p = p0 + (wave * kBpNB + nb) * 32 + col;
         yo[nb] = kBufferOutOfRange;
         xo[nb] = -1;
+        ih0[nb] = iw0[nb] = 0;
         if (p < a.npix) {
             const int32_t b = p / HWo, hw = p - b * HWo;
+            const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+            ih0[nb] = oh * a.sh;
+            iw0[nb] = ow * a.sw;
             yo[nb] = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
-            xo[nb] = int64_t(b) * a.m * HWo + hw;
+            xo[nb] = int64_t(b) * a.m * HWi + int64_t(ih0[nb]) * a.W + iw0[nb];
         }
     }
     const uint32_t chb = uint32_t(HWo) * 4;   // bytes between dY channels
@@ -236,7 +251,236 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
             const int32_t c = c0 + M::row(lane, r);
-            if (c < a.m) store_out(&dx[xo[nb] + int64_t(c) * HWo], acc[nb][r]);
+            if (c < a.m) store_out(&dx[xo[nb] + int64_t(c) * HWi], acc[nb][r]);
+        }
+    }
+    // A strided layer reads only (oh * sh, ow * sw): the rest of that
+    // sh x sw block of dX (clipped to the image) gets no gradient.  The blocks
+    // of all output pixels cover the input exactly once (Ho * sh >= H).
+    if (a.sh * a.sw > 1) {
+#pragma unroll
+        for (int nb = 0; nb < kBpNB; ++nb) {
+            if (xo[nb] < 0) continue;
+            const int32_t dhe = min(a.sh, a.H - ih0[nb]), dwe = min(a.sw, a.W - iw0[nb]);
+#pragma unroll
+            for (int r = 0; r < M::ACC; ++r) {
+                const int32_t c = c0 + M::row(lane, r);
+                if (c >= a.m) continue;
+                float* q = &dx[xo[nb] + int64_t(c) * HWi];
+                for (int32_t dh = 0; dh < dhe; ++dh)
+                    for (int32_t dw = 0; dw < dwe; ++dw)
+                        if (dh != 0 || dw != 0) store_out(q + int64_t(dh) * a.W + dw, 0.f);
+            }
+        }
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Input gradient of a 3x3 layer, stride 1 or 2, any padding: for every tap
+// (q, r) the contraction above with dY read at the positions the tap maps the
+// input pixel to,
+//     dX[c][ih][iw] = sum_g sum_{i < N} sum_{q, r} Wt_g[c][i][q][r] * dY[gN + i][oh][ow],
+//     oh = (ih + ph - q) / s, ow = (iw + pw - r) / s,
+// the term absent where a division is inexact or (oh, ow) lies outside the
+// output.  Same workgroup shape as the 1x1 kernel (32 input channels x 256
+// input pixels, a wave per 32-pixel block, rows = channels); each col-group
+// is multiplied for its nine taps in turn.  Its 32 x (N x 9) tile of
+// Omega-bar's transpose (row c: the kept block's D row, taps innermost) is
+// copied from D straight into LDS between two barriers (rows of channels the
+// col-group does not keep read zeros); the dY values of the next tap are
+// loaded while this tap multiplies.  At stride 2 an input pixel takes 1, 2 or
+// 4 of the nine taps; the others read zeros.  Each output element is stored
+// once: deterministic.
+// ---------------------------------------------------------------------------
+
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int Count, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, Count>{});
+}
+
+template <int N, int SD>
+__global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_k3(ConvArgs a, const float* __restrict__ dy,
+                                                           float* __restrict__ dx) {
+    typedef PwMfma<32> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int KK = 9;
+    constexpr int S = N / 2;                            // MFMA steps per tap
+    constexpr int RW = N * KK;                          // floats of a D row
+    constexpr int AP = RW + 1;                          // LDS pitch of a tile row
+    static_assert(32 % kBpWaves == 0 && RW >= 64, "tile rows split over waves, pieces of 64 floats");
+    __shared__ int32_t sFirst[kBpMaxG];                 // first block of col-group g in the tile
+    __shared__ uint32_t sMask[kBpMaxG];                 // bit k: g keeps channel c0 + k
+    __shared__ int32_t sGl[kBpMaxG];                    // col-groups with a kept block in the tile
+    __shared__ int32_t sCnt[kBpWaves];
+    __shared__ float sA[32 * AP];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t c0 = int32_t(blockIdx.y) * 32;
+    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first input pixel
+
+    // ---- Index prologue: thread g < G finds col-group g's run of blocks in
+    // [c0, c0 + 32): entries first, first + 1, ... in ascending channel order,
+    // so channel c0 + k is block first + popcount(mask below bit k).
+    const int32_t g = tid;
+    bool any = false;
+    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(a.t * 4), kRawBufferFlags);
+    if (g < a.G) {
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        const int32_t first = run_first(rI, zb, ze, c0);
+        uint32_t mask = 0;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = first + k;
+            const int32_t c = e < ze ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)) : INT32_MAX;
+            if (c < c0 + 32 && c < a.m) mask |= 1u << (c - c0);
+        }
+        sFirst[g] = first;
+        sMask[g] = mask;
+        any = mask != 0;
+    }
+    const uint64_t bal = __ballot(any);
+    if (lane == 0) sCnt[wave] = __builtin_popcountll(bal);
+    __syncthreads();
+    int32_t base = 0, ng = 0;
+#pragma unroll
+    for (int w = 0; w < kBpWaves; ++w) {
+        base += w < wave ? sCnt[w] : 0;
+        ng += sCnt[w];
+    }
+    if (any) sGl[base + __builtin_popcountll(bal & ((uint64_t(1) << lane) - 1))] = g;
+    __syncthreads();
+
+    // ---- Lane roles.  A: row (input channel c0 + lane % 32), entry parity
+    // kk.  B: input pixel lane % 32 of the wave's block, output channel 2s + kk.
+    const int col = lane & 31, kk = lane >> 5;
+    const int32_t HWo = a.HWo, HWi = a.H * a.W;
+    const int32_t batch = a.npix / HWo;
+    const int32_t ybytes = int32_t(int64_t(batch) * a.n * HWo * 4);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(ybytes), kRawBufferFlags);
+    const uint32_t chb = uint32_t(HWo) * 4;   // bytes between dY channels
+    const int32_t p = p0 + wave * 32 + col;
+    int64_t xo = -1;                          // dX element offset at channel 0 (or -1)
+    uint32_t yk[KK];                          // per tap: byte offset of dY at channel kk (or out of range)
+    {
+        const bool in = p < batch * HWi;
+        const int32_t b = in ? p / HWi : 0, hw = p - b * HWi;
+        const int32_t ih = hw / a.W, iw = hw - ih * a.W;
+        if (in) xo = int64_t(b) * a.m * HWi + hw;
+        const int64_t ybase = int64_t(b) * a.n * HWo;
+        int32_t orow[3], ocol[3];
+        bool vrow[3], vcol[3];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const int32_t th = ih + a.ph - q, tw = iw + a.pw - q;
+            vrow[q] = th >= 0 && (SD == 1 || (th & 1) == 0) && th / SD < a.Ho;
+            vcol[q] = tw >= 0 && (SD == 1 || (tw & 1) == 0) && tw / SD < a.Wo;
+            orow[q] = (th / SD) * a.Wo;
+            ocol[q] = tw / SD;
+        }
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+#pragma unroll
+            for (int r = 0; r < 3; ++r)
+                yk[q * 3 + r] = in && vrow[q] && vcol[r]
+                                    ? uint32_t((ybase + orow[q] + ocol[r]) * 4) + uint32_t(kk) * chb
+                                    : kBufferOutOfRange;
+    }
+    // The step's output channel pair in the scalar offset (uniform, in range
+    // for every row below n); a row past n (ragged last col-group) takes an
+    // out-of-range vector offset instead.  One path, no branch: the loads of
+    // consecutive taps stay in one counted sequence.
+    auto load_b = [&](float (&bv)[S], int32_t gg, int tap) __attribute__((always_inline)) {
+        const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
+        const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                rY, int32_t(2 * s < lim ? yk[tap] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+    };
+    // Tile of col-group gg: row c (channel c0 + c) is D row z (RW floats) if
+    // the col-group keeps the channel at block z, else zeros (an out-of-range
+    // offset).  Copied in 64-float pieces, the last one of a row overlapping
+    // the one before; wave w copies rows 4w .. 4w + 3.
+    constexpr int C = (RW + 63) / 64;                   // pieces per row
+    const v4i32 rD = buffer_rsrc(a.D, int32_t(int64_t(a.t) * RW * 4));
+    auto copy_a = [&](int32_t gg) __attribute__((always_inline)) {
+        const int32_t first = __builtin_amdgcn_readfirstlane(sFirst[gg]);
+        const uint32_t mask = __builtin_amdgcn_readfirstlane(sMask[gg]);
+#pragma unroll
+        for (int rr = 0; rr < 32 / kBpWaves; ++rr) {
+            const int32_t row = wave * (32 / kBpWaves) + rr;
+            const bool kept = (mask >> row) & 1;
+            const int32_t z = first + __builtin_popcount(mask & ((1u << row) - 1));
+#pragma unroll
+            for (int u = 0; u < C; ++u) {
+                const int j0 = u * 64 < RW - 64 ? u * 64 : RW - 64;
+                copy4_to_lds(rD, (const lds_char*)(sA + row * AP + j0),
+                             kept ? (z * RW + j0 + lane) * 4 : int32_t(kBufferOutOfRange), 0);
+            }
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    auto multiply = [&](int tap, const float (&bv)[S]) __attribute__((always_inline)) {
+        const float* ar = &sA[col * AP + kk * KK + tap];
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc = M::step(ar[2 * s * KK], bv[s], acc);
+    };
+
+    if (ng > 0) {
+        float b0[S], b1[S];
+        copy_a(sGl[0]);
+        load_b(b0, sGl[0], 0);
+        vm_wait<0>();
+        __syncthreads();
+        // Step (col-group j, tap T) multiplies register set (j * 9 + T) % 2
+        // and loads the next step's dY values into the other one.
+        auto group = [&](int32_t j, auto par) __attribute__((always_inline)) {
+            const int32_t gg = sGl[j];
+            const bool more = j + 1 < ng;
+            const int32_t gn = more ? sGl[j + 1] : gg;
+            static_for<KK>([&](auto T) {
+                constexpr bool odd = ((decltype(par)::value + decltype(T)::value) & 1) != 0;
+                float (&cur)[S] = odd ? b1 : b0;
+                float (&nxt)[S] = odd ? b0 : b1;
+                if (T + 1 < KK)
+                    load_b(nxt, gg, T + 1 < KK ? T + 1 : 0);
+                else if (more)
+                    load_b(nxt, gn, 0);
+                multiply(T, cur);
+            });
+            if (more) {
+                __syncthreads();   // every wave is done with the tile
+                copy_a(gn);
+                vm_wait<0>();
+                __syncthreads();
+            }
+        };
+        for (int32_t j = 0; j < ng; j += 2) {
+            group(j, std::integral_constant<int, 0>{});
+            if (j + 1 >= ng) break;
+            group(j + 1, std::integral_constant<int, KK & 1>{});
+        }
+    }
+
+    // ---- Store: MFMA (row, col) -> dX channel c0 + row at the lane's pixel
+    // (zero for pixels no tap reaches).
+    if (xo >= 0) {
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) {
+            const int32_t c = c0 + M::row(lane, r);
+            if (c < a.m) store_out(&dx[xo + int64_t(c) * HWi], acc[r]);
         }
     }
 }
@@ -246,24 +490,42 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
     if (wdt != ONEXN_F32 || dxdt != ONEXN_F32) return false;
     if (a.N != 16 && a.N != 32) return false;
-    if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
+    const bool pw = a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0;                       // any stride
+    const bool k3 = a.kh == 3 && a.kw == 3 && a.sh == a.sw && (a.sh == 1 || a.sh == 2);   // any padding
+    if (!pw && !k3) return false;
+    if (k3 && int64_t(a.t) * a.N * 9 * 4 >= (int64_t(1) << 31)) return false;   // D through a buffer
     if (a.G > kBpMaxG) return false;
     if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31)) return false;   // 32-bit buffer offsets
     return true;
 }
 
 onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hipStream_t s) {
-    const int64_t ptiles = (int64_t(a.npix) + kBpPix - 1) / kBpPix;
+    // The 1x1 kernel walks the output pixels, the 3x3 one the input pixels.
+    const bool k3 = a.kh == 3;
+    const int64_t pix = k3 ? int64_t(a.npix / a.HWo) * a.H * a.W : int64_t(a.npix);
+    const int64_t ptiles = (pix + kBpPix - 1) / kBpPix;
     const int64_t ctiles = (int64_t(a.m) + 31) / 32;
     if (ptiles > INT32_MAX || ctiles > 65535)
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_data: grid out of range");
     const dim3 grid{uint32_t(ptiles), uint32_t(ctiles), 1};
-    if (a.N == 32)
-        hipLaunchKernelGGL(bwd_data_pw<32>, grid, dim3(kBpThreads), 0, s, a, static_cast<const float*>(dy),
-                           static_cast<float*>(dx));
-    else
-        hipLaunchKernelGGL(bwd_data_pw<16>, grid, dim3(kBpThreads), 0, s, a, static_cast<const float*>(dy),
-                           static_cast<float*>(dx));
+    const float* y = static_cast<const float*>(dy);
+    float* x = static_cast<float*>(dx);
+    if (!k3) {
+        if (a.N == 32)
+            hipLaunchKernelGGL(bwd_data_pw<32>, grid, dim3(kBpThreads), 0, s, a, y, x);
+        else
+            hipLaunchKernelGGL(bwd_data_pw<16>, grid, dim3(kBpThreads), 0, s, a, y, x);
+    } else if (a.sh == 1) {
+        if (a.N == 32)
+            hipLaunchKernelGGL((bwd_data_k3<32, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
+        else
+            hipLaunchKernelGGL((bwd_data_k3<16, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
+    } else {
+        if (a.N == 32)
+            hipLaunchKernelGGL((bwd_data_k3<32, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
+        else
+            hipLaunchKernelGGL((bwd_data_k3<16, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
+    }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_data: launch failed: %s", hipGetErrorString(err));
     return ONEXN_OK;

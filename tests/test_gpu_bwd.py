@@ -50,6 +50,20 @@ CASES = [  # (n, m, k, stride, pad, B, H, W, N)
     (40, 70, 1, 1, 0, 2, 10, 10, 16),   # three channel tiles, the last partial
     (96, 300, 1, 1, 0, 1, 9, 9, 32),    # col-groups of up to 300 blocks (narrowing rounds)
     (48, 1100, 1, 1, 0, 1, 5, 4, 16),   # col-groups longer than 1024 blocks
+    # 1x1 strided at N = 16 / 32: the matrix-core kernel, zeros off the stride grid
+    (80, 45, 1, 2, 0, 2, 9, 11, 32),    # odd map: the last block row/column clipped
+    (40, 70, 1, 3, 0, 1, 10, 8, 16),
+    # 3x3 at N = 16 / 32 (stride 1 and 2, padding 0-2): the matrix-core tap kernel
+    (64, 100, 3, 1, 1, 1, 8, 8, 32),    # four channel tiles, the last partial
+    (48, 40, 3, 1, 0, 2, 9, 10, 32),
+    (36, 33, 3, 2, 2, 1, 11, 12, 16),   # ragged last col-group
+    (300, 40, 3, 2, 1, 1, 9, 9, 32),    # ten col-groups, the last ragged
+    (32, 20, 3, 1, 2, 3, 5, 4, 16),     # padding wider than the map's margin
+    # at most four input channels: the one-lane-per-pixel input gradient
+    (20, 4, 3, 1, 1, 2, 9, 7, 4),
+    (33, 1, 5, 3, 2, 1, 11, 13, 8),     # stride 3, output channels not a multiple of 8
+    (64, 2, 1, 2, 0, 2, 9, 9, 16),
+    (16, 3, 7, 2, 3, 1, 9, 150, 16),    # stem-like, two 64-column chunks per residue class
 ]
 
 
