@@ -569,7 +569,7 @@ __global__ void __launch_bounds__(256) bw_zero(float* __restrict__ p, int64_t n)
     for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) p[i] = 0.f;
 }
 
-template <int N>
+template <int N, bool KT>
 __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const float* __restrict__ x,
                                                              const float* __restrict__ dy,
                                                              float* __restrict__ dD, int32_t tiles_per_g,
@@ -585,17 +585,19 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // Work item: (col-group, tile of N kept blocks, tap, pixel range).
+    // Work item: (col-group, tile of N (block, tap) pairs, pixel range).  The
+    // col-group's pairs are numbered tap-major, pair = tap * cnt + k for its
+    // k-th kept block, so a tile is N blocks of one tap where the col-group
+    // keeps many, and several taps of its few blocks where it keeps few.
     const int32_t item = blockIdx.x;
     const int32_t split = item % nsplit;
-    const int32_t tap = (item / nsplit) % a.KK;            // kernel tap (q, r) of the work item
-    const int32_t gt = item / nsplit / a.KK;
-    const int32_t q = tap / a.kw, r = tap - q * a.kw;
+    const int32_t gt = item / nsplit;
     const int32_t g = gt / tiles_per_g, tile = gt - g * tiles_per_g;
     int32_t zb, ze;
     group_range(a, g, zb, ze);
-    const int32_t e0 = zb + tile * N;
-    if (e0 >= ze) return;                      // (uniform: the col-group has fewer tiles)
+    const int32_t cnt = ze - zb, npairs = cnt * a.KK;
+    const int32_t pr0 = tile * N;              // first pair of the tile
+    if (pr0 >= npairs) return;                 // (uniform: the col-group has fewer tiles)
     const int32_t pb = int32_t(int64_t(a.npix) * split / nsplit);
     const int32_t pe = int32_t(int64_t(a.npix) * (split + 1) / nsplit);
 
@@ -611,37 +613,60 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
     const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
         kRawBufferFlags);
-    // Row offsets (bytes, pixel part excluded): the tile's blocks' input
-    // channels and the col-group's output channels; a block past the
-    // col-group, a channel outside [0, m) or a row past n reads zeros.
+    // Per row of the thread: the pair's input channel (bytes) and tap, and
+    // the col-group's output channel (bytes); a pair past the col-group's, a
+    // channel outside [0, m) or a row past n reads zeros.
     uint32_t xr[RPT], yr[RPT];
+    int32_t tq[RPT];                           // tap row q << 8 | tap column r, or -1
+    uint32_t valid = 0;                        // bit j: row j is a pair with a channel in [0, m)
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
         const int32_t r = r0 + RS * j;
-        const int32_t e = e0 + r;
-        const int32_t c = e < ze ? a.I[e] : -1;
-        xr[j] = uint32_t(c) < uint32_t(a.m) ? uint32_t(c) * xchb : kBufferOutOfRange;
+        const int32_t pr = pr0 + r;
+        const int32_t tap = pr < npairs ? pr / cnt : 0;
+        const int32_t c = pr < npairs ? a.I[zb + pr - tap * cnt] : -1;
+        const bool ok = uint32_t(c) < uint32_t(a.m);
+        xr[j] = ok ? uint32_t(c) * xchb : 0u;
+        tq[j] = ok ? (tap / a.kw) << 8 | (tap % a.kw) : -1;
+        valid |= uint32_t(ok) << j;
         const int32_t o = g * N + r;
         yr[j] = o < a.n ? uint32_t(o) * chb : kBufferOutOfRange;
     }
+    // A 1x1 layer (KT false) has the one tap (0, 0): one bounds check per
+    // pixel.  Otherwise each row checks its own shift (a version that took a
+    // one-check path for tiles within one tap needed 188 registers, against
+    // 148).
     float vx[RPT], vy[RPT];
     auto load = [&](int32_t p0) __attribute__((always_inline)) {
         const int32_t p = p0 + px;
-        uint32_t bx = kBufferOutOfRange, by = kBufferOutOfRange;
-        if (p < pe) {
-            // Output pixel p; its input pixel under tap (q, r) (outside the
-            // image: zero padding, read as zeros).
-            const int32_t b = p / HWo, hw = p - b * HWo;
-            const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
-            const int32_t ih = oh * a.sh - a.ph + q, iw = ow * a.sw - a.pw + r;
-            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
-                bx = uint32_t((int64_t(b) * a.m * HW + int64_t(ih) * a.W + iw) * 4);
-            by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
-        }
+        const bool in = p < pe;
+        // Output pixel p; under row j's tap (q, r) it reads input pixel
+        // (oh*sh - ph + q, ow*sw - pw + r), zero outside the image (padding).
+        const int32_t b = in ? p / HWo : 0, hw = p - b * HWo;
+        const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+        const int32_t ih0 = oh * a.sh - a.ph, iw0 = ow * a.sw - a.pw;
+        const uint32_t bx = uint32_t((int64_t(b) * a.m * HW + int64_t(ih0) * a.W + iw0) * 4);
+        const uint32_t by = in ? uint32_t((int64_t(b) * a.n * HWo + hw) * 4) : kBufferOutOfRange;
+        if (!KT) {
+            const bool okp = in && uint32_t(ih0) < uint32_t(a.H) && uint32_t(iw0) < uint32_t(a.W);
 #pragma unroll
-        for (int j = 0; j < RPT; ++j) {
-            vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rX, int32_t(bx + xr[j]), 0, 0));
-            vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
+            for (int j = 0; j < RPT; ++j) {
+                const bool ok = okp && ((valid >> j) & 1);
+                vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rX, int32_t(ok ? bx + xr[j] : kBufferOutOfRange), 0, 0));
+                vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) {
+                const int32_t q = tq[j] >> 8, r = tq[j] & 0xff;
+                const bool ok = in && tq[j] >= 0 && uint32_t(ih0 + q) < uint32_t(a.H) &&
+                                uint32_t(iw0 + r) < uint32_t(a.W);
+                const uint32_t xo = bx + xr[j] + uint32_t(q * a.W + r) * 4;
+                vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rX, int32_t(ok ? xo : kBufferOutOfRange), 0, 0));
+                vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
+            }
         }
     };
     auto put = [&]() __attribute__((always_inline)) {
@@ -681,12 +706,13 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
 #pragma unroll
     for (int r = 0; r < M::ACC; ++r)
         acc[r] = ((sR[0][r * 64 + lane] + sR[1][r * 64 + lane]) + sR[2][r * 64 + lane]) + sR[3][r * 64 + lane];
-    // MFMA (row, col): block e0 + row, block row col.
+    // MFMA (row, col): pair pr0 + row (block zb + k, tap), block row col.
 #pragma unroll
     for (int r = 0; r < M::ACC; ++r) {
-        const int32_t e = e0 + M::row(lane, r);
-        if (e >= ze) continue;
-        float* dst = dD + (int64_t(e) * N + rc) * a.KK + tap;
+        const int32_t pr = pr0 + M::row(lane, r);
+        if (pr >= npairs) continue;
+        const int32_t tap = pr / cnt;
+        float* dst = dD + (int64_t(zb + pr - tap * cnt) * N + rc) * a.KK + tap;
         if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
         else *dst = acc[r];
     }
@@ -704,14 +730,15 @@ bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
 }
 
 onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
-    const int64_t tiles_per_g = (int64_t(a.m) + a.N - 1) / a.N;   // a col-group keeps at most m blocks
-    const int64_t tiles = ((int64_t(a.t) + a.N - 1) / a.N + a.G) * a.KK;   // (tile, tap) items with blocks, at most
+    // A col-group keeps at most m blocks: m * KK pairs.
+    const int64_t tiles_per_g = (int64_t(a.m) * a.KK + a.N - 1) / a.N;
+    const int64_t tiles = (int64_t(a.t) * a.KK + a.N - 1) / a.N + a.G;   // tiles with pairs, at most
     // Pixel ranges per tile: enough workgroups for four per CU, each range
     // at least 1024 pixels; one range where the tiles suffice (stored, not added).
     int64_t nsplit = (4 * int64_t(device_cu_count()) + tiles - 1) / tiles;
     nsplit = std::max<int64_t>(1, std::min<int64_t>(nsplit, a.npix / 1024));
     if (tuning(kTuneBwdSplit) >= 1) nsplit = tuning(kTuneBwdSplit);
-    const int64_t grid = int64_t(a.G) * tiles_per_g * a.KK * nsplit;
+    const int64_t grid = int64_t(a.G) * tiles_per_g * nsplit;
     if (grid < 1 || grid > INT32_MAX)
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_weight: grid out of range");
     if (nsplit > 1) {
@@ -721,14 +748,18 @@ onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* 
         if (zerr != hipSuccess)
             return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(zerr));
     }
-    if (a.N == 32)
-        hipLaunchKernelGGL(bwd_weight_pw<32>, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a,
-                           static_cast<const float*>(x), static_cast<const float*>(dy), dD, int32_t(tiles_per_g),
-                           int32_t(nsplit));
-    else
-        hipLaunchKernelGGL(bwd_weight_pw<16>, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a,
-                           static_cast<const float*>(x), static_cast<const float*>(dy), dD, int32_t(tiles_per_g),
-                           int32_t(nsplit));
+    // (A 1x1 layer's tiles all lie within its one tap: no per-row shifts.)
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a, static_cast<const float*>(x),
+                           static_cast<const float*>(dy), dD, int32_t(tiles_per_g), int32_t(nsplit));
+    };
+    if (a.N == 32) {
+        if (a.KK > 1) go(bwd_weight_pw<32, true>);
+        else go(bwd_weight_pw<32, false>);
+    } else {
+        if (a.KK > 1) go(bwd_weight_pw<16, true>);
+        else go(bwd_weight_pw<16, false>);
+    }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(err));
     return ONEXN_OK;
