@@ -1,5 +1,5 @@
-// Input gradient of a 1x1 (stride 1, no padding) 1xN-pruned convolution on
-// matrix cores: fp32, NCHW, N in {16, 32}.
+// Input gradient of 1x1 (any stride, no padding) and 3x3 (stride 1 or 2)
+// 1xN-pruned convolutions on matrix cores: fp32, NCHW, N in {16, 32}.
 //
 // Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
 // (arXiv 2105.14713), Sec. 3.4 (Eq. 7 with Omega-bar, stored as Eq. 8's BSR)
@@ -9,7 +9,8 @@
 //     Wt_g[c][i] = D[z][i] if col-group g keeps input channel c at block z,
 //                  else 0,
 // a dense contraction over the output channels with Omega-bar's transpose
-// as the left operand.
+// as the left operand (a strided layer's dY pixel feeds input (oh*sh, ow*sw)
+// only).
 //
 // Work.  A workgroup of eight waves computes 32 input channels x 256 pixels
 // (each wave one 32-pixel column block) with v_mfma_f32_32x32x2f32: row =
@@ -19,11 +20,16 @@
 //  - Index.  I ascends within a col-group, so the blocks of a col-group whose
 //    channel falls in [c0, c0 + 32) are one run.  In a prologue each thread
 //    finds one col-group's run by narrowing with 32 samples at a time (one
-//    round of independent loads per 32x narrowing), then records the run's
-//    block per channel in LDS.
-//  - A.  The 32 x N tile Wt_g is built in LDS (double-buffered, one
-//    col-group ahead; rows are the runs' D rows, zero where a channel is not
-//    kept) and read one float per lane and step.
+//    round of independent loads per 32x narrowing) and records its first
+//    block and a mask of the channels it keeps: channel c0 + k is block
+//    first + popcount(mask below bit k).
+//  - A.  The 32 x N tiles Wt_g of eight col-groups at a time are copied from
+//    D straight into one LDS buffer between two barriers (rows of channels a
+//    col-group does not keep read zeros through an out-of-range offset), so
+//    no registers hold tiles in flight and a wave multiplies 8 x N/2 steps
+//    per barrier pair (a version with one col-group's tile per barrier,
+//    built in LDS one col-group ahead through registers, was 2-16 % slower
+//    per layer).
 //  - B.  dY rows gN .. gN+N-1 at the wave's pixels, loaded into registers
 //    one col-group ahead.
 // Every output element is written once, by one lane, after a fixed-order
@@ -39,8 +45,7 @@ namespace {
 
 constexpr int kBpWaves = 8;
 constexpr int kBpThreads = 64 * kBpWaves;
-constexpr int kBpNB = 1;                                // 32-pixel column blocks per wave
-constexpr int kBpPix = kBpWaves * kBpNB * 32;           // pixels per workgroup
+constexpr int kBpPix = kBpWaves * 32;                   // pixels per workgroup (a 32-pixel block per wave)
 constexpr int kBpMaxG = 256;                            // col-groups (one prologue thread each)
 
 // First entry in [zb, ze) of a col-group whose input channel is >= c0 (ze if
@@ -71,210 +76,6 @@ __device__ __forceinline__ int32_t run_first(__amdgpu_buffer_rsrc_t rI, int32_t 
     }
     return lo + below;
 }
-
-template <int N>
-__global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_pw(ConvArgs a, const float* __restrict__ dy,
-                                                           float* __restrict__ dx) {
-    typedef PwMfma<32> M;
-    typedef typename M::acc_t acc_t;
-    constexpr int S = N / 2;                            // MFMA steps per col-group
-    constexpr int AP = N + 1;                           // LDS pitch of a Wt row (floats)
-    __shared__ int32_t sZ[kBpMaxG][32];                 // block of (g, channel), or -1
-    __shared__ int32_t sGl[kBpMaxG];                    // col-groups with a kept block in the tile
-    __shared__ int32_t sCnt[kBpWaves];
-    __shared__ float sA[2][32 * AP];
-
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t c0 = int32_t(blockIdx.y) * 32;
-    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;
-
-    // ---- Index prologue: thread g < G finds the run of col-group g.  (I through
-    // a range-checked buffer: one 32-bit offset register per load.)
-    const int32_t g = tid;
-    bool any = false;
-    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(a.t * 4), kRawBufferFlags);
-    auto ld_i = [&](int32_t e) { return int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)); };
-    if (g < a.G) {
-        int32_t zb, ze;
-        group_range(a, g, zb, ze);
-        const int32_t first = run_first(rI, zb, ze, c0);
-        // The run: up to 32 entries from first whose channel is below c0 + 32.
-#pragma unroll
-        for (int k = 0; k < 32; ++k) sZ[g][k] = -1;
-#pragma unroll
-        for (int k = 0; k < 32; ++k) {
-            const int32_t e = first + k;
-            const int32_t c = e < ze ? ld_i(e) : INT32_MAX;
-            if (c >= c0 && c < c0 + 32 && c < a.m) {
-                sZ[g][c - c0] = e;
-                any = true;
-            }
-        }
-    }
-    // Compact the col-groups with a kept block, in order.
-    const uint64_t bal = __ballot(any);
-    if (lane == 0) sCnt[wave] = __builtin_popcountll(bal);
-    __syncthreads();
-    int32_t base = 0, ng = 0;
-#pragma unroll
-    for (int w = 0; w < kBpWaves; ++w) {
-        base += w < wave ? sCnt[w] : 0;
-        ng += sCnt[w];
-    }
-    if (any) sGl[base + __builtin_popcountll(bal & ((uint64_t(1) << lane) - 1))] = g;
-    __syncthreads();
-
-    // ---- Lane roles.  A: row (input channel c0 + lane % 32), entry parity
-    // kk.  B: pixel column lane % 32 of each block, output channel 2s + kk.
-    const int col = lane & 31, kk = lane >> 5;
-    const int32_t HWo = a.HWo, HWi = a.H * a.W;
-    const int32_t ybytes = int32_t(int64_t(a.npix / HWo) * a.n * HWo * 4);
-    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(ybytes), kRawBufferFlags);
-    uint32_t yo[kBpNB];   // byte offset of the pixel's dY value at output channel 0 (or out of range)
-    int64_t xo[kBpNB];    // element offset of its dX value at channel 0 (or -1)
-    int32_t ih0[kBpNB], iw0[kBpNB];   // the input position it reads (oh * sh, ow * sw)
-#pragma unroll
-    for (int nb = 0; nb < kBpNB; ++nb) {
-        const int32_t p = p0 + (wave * kBpNB + nb) * 32 + col;
-        yo[nb] = kBufferOutOfRange;
-        xo[nb] = -1;
-        ih0[nb] = iw0[nb] = 0;
-        if (p < a.npix) {
-            const int32_t b = p / HWo, hw = p - b * HWo;
-            const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
-            ih0[nb] = oh * a.sh;
-            iw0[nb] = ow * a.sw;
-            yo[nb] = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
-            xo[nb] = int64_t(b) * a.m * HWi + int64_t(ih0[nb]) * a.W + iw0[nb];
-        }
-    }
-    const uint32_t chb = uint32_t(HWo) * 4;   // bytes between dY channels
-    // The lane's part of the offset in the vector offset (range-checked: a
-    // pixel past the last image reads zeros), the step's output channel pair
-    // in the scalar offset; in a ragged last col-group a row past n takes an
-    // out-of-range vector offset instead.
-    uint32_t yk[kBpNB];
-#pragma unroll
-    for (int nb = 0; nb < kBpNB; ++nb) yk[nb] = yo[nb] + uint32_t(kk) * chb;
-    auto load_b = [&](float (&bv)[S][kBpNB], int32_t gg) __attribute__((always_inline)) {
-        const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
-        if (ob + N <= a.n) {
-#pragma unroll
-            for (int s = 0; s < S; ++s)
-#pragma unroll
-                for (int nb = 0; nb < kBpNB; ++nb)
-                    bv[s][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                        rY, int32_t(yk[nb]), int32_t(uint32_t(ob + 2 * s) * chb), 0));
-        } else {
-#pragma unroll
-            for (int s = 0; s < S; ++s)
-#pragma unroll
-                for (int nb = 0; nb < kBpNB; ++nb) {
-                    const bool ok = ob + 2 * s + kk < a.n;
-                    bv[s][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                        rY, int32_t(ok ? yk[nb] + uint32_t(ob + 2 * s) * chb : kBufferOutOfRange), 0, 0));
-                }
-        }
-    };
-    // The Wt tile of col-group gg: thread t holds elements t, t + 256, ...
-    // of the 32 x N tile (row-major), fetched before the current col-group's
-    // multiplies and written after them.
-    constexpr int AE = 32 * N / kBpThreads;   // tile elements per thread
-    const float* __restrict__ D = static_cast<const float*>(a.D);
-    auto fetch_a = [&](float (&av)[AE], int32_t gg) __attribute__((always_inline)) {
-#pragma unroll
-        for (int k = 0; k < AE; ++k) {
-            const int32_t e = tid + k * kBpThreads, r = e / N, i = e - r * N;
-            const int32_t z = sZ[gg][r];
-            av[k] = z >= 0 ? D[int64_t(z) * N + i] : 0.f;
-        }
-    };
-    auto put_a = [&](const float (&av)[AE], int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int k = 0; k < AE; ++k) {
-            const int32_t e = tid + k * kBpThreads, r = e / N, i = e - r * N;
-            sA[buf][r * AP + i] = av[k];
-        }
-    };
-
-    acc_t acc[kBpNB];
-#pragma unroll
-    for (int nb = 0; nb < kBpNB; ++nb)
-#pragma unroll
-        for (int r = 0; r < M::ACC; ++r) acc[nb][r] = 0.f;
-
-    auto multiply = [&](int buf, const float (&bv)[S][kBpNB]) __attribute__((always_inline)) {
-        const float* ar = &sA[buf][col * AP + kk];
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-            const float av = ar[2 * s];
-#pragma unroll
-            for (int nb = 0; nb < kBpNB; ++nb) acc[nb] = M::step(av, bv[s][nb], acc[nb]);
-        }
-    };
-
-    if (ng > 0) {
-        float b0[S][kBpNB], b1[S][kBpNB], af[AE];
-        fetch_a(af, sGl[0]);
-        load_b(b0, sGl[0]);
-        put_a(af, 0);
-        __syncthreads();
-        // Col-group j is multiplied from LDS buffer j % 2 and register set
-        // j % 2; col-group j + 1's operands are fetched first.
-        for (int32_t j = 0; j < ng; j += 2) {
-            if (j + 1 < ng) {
-                fetch_a(af, sGl[j + 1]);
-                load_b(b1, sGl[j + 1]);
-            }
-            multiply(0, b0);
-            if (j + 1 >= ng) break;
-            put_a(af, 1);
-            __syncthreads();
-            if (j + 2 < ng) {
-                fetch_a(af, sGl[j + 2]);
-                load_b(b0, sGl[j + 2]);
-            }
-            multiply(1, b1);
-            if (j + 2 < ng) put_a(af, 0);
-            __syncthreads();
-        }
-    }
-
-    // ---- Store: MFMA (row, col) of block nb -> dX channel c0 + row, the
-    // block's pixel col.
-#pragma unroll
-    for (int nb = 0; nb < kBpNB; ++nb) {
-        if (xo[nb] < 0) continue;
-#pragma unroll
-        for (int r = 0; r < M::ACC; ++r) {
-            const int32_t c = c0 + M::row(lane, r);
-            if (c < a.m) store_out(&dx[xo[nb] + int64_t(c) * HWi], acc[nb][r]);
-        }
-    }
-    // A strided layer reads only (oh * sh, ow * sw): the rest of that
-    // sh x sw block of dX (clipped to the image) gets no gradient.  The blocks
-    // of all output pixels cover the input exactly once (Ho * sh >= H).
-    if (a.sh * a.sw > 1) {
-#pragma unroll
-        for (int nb = 0; nb < kBpNB; ++nb) {
-            if (xo[nb] < 0) continue;
-            const int32_t dhe = min(a.sh, a.H - ih0[nb]), dwe = min(a.sw, a.W - iw0[nb]);
-#pragma unroll
-            for (int r = 0; r < M::ACC; ++r) {
-                const int32_t c = c0 + M::row(lane, r);
-                if (c >= a.m) continue;
-                float* q = &dx[xo[nb] + int64_t(c) * HWi];
-                for (int32_t dh = 0; dh < dhe; ++dh)
-                    for (int32_t dw = 0; dw < dwe; ++dw)
-                        if (dh != 0 || dw != 0) store_out(q + int64_t(dh) * a.W + dw, 0.f);
-            }
-        }
-    }
-}
-
 
 // ---------------------------------------------------------------------------
 // Input gradient of a 3x3 layer, stride 1 or 2, any padding: for every tap
@@ -485,6 +286,171 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// The 1x1 kernel (see the top of the file).
+// ---------------------------------------------------------------------------
+
+template <int N>
+__global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_pw(ConvArgs a, const float* __restrict__ dy,
+                                                            float* __restrict__ dx) {
+    typedef PwMfma<32> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int CG = 8;                               // col-groups per stage
+    constexpr int S = N / 2;                            // MFMA steps per col-group
+    constexpr int RW = CG * N;                          // floats of a staged row
+    constexpr int AP = RW + 1;                          // LDS pitch of a staged row
+    constexpr int CPR = RW / 64;                        // 64-float copies per row
+    static_assert(RW % 64 == 0 && 32 % kBpWaves == 0, "whole copies, rows split over waves");
+    __shared__ int32_t sFirst[kBpMaxG];                 // first block of col-group g in the tile
+    __shared__ uint32_t sMask[kBpMaxG];                 // bit k: g keeps channel c0 + k
+    __shared__ int32_t sGl[kBpMaxG];                    // col-groups with a kept block in the tile
+    __shared__ int32_t sCnt[kBpWaves];
+    __shared__ float sA[32 * AP];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t c0 = int32_t(blockIdx.y) * 32;
+    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first output pixel
+
+    // ---- Index prologue (as in the 3x3 kernel).
+    const int32_t g = tid;
+    bool any = false;
+    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(a.t * 4), kRawBufferFlags);
+    if (g < a.G) {
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        const int32_t first = run_first(rI, zb, ze, c0);
+        uint32_t mask = 0;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = first + k;
+            const int32_t c = e < ze ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)) : INT32_MAX;
+            if (c < c0 + 32 && c < a.m) mask |= 1u << (c - c0);
+        }
+        sFirst[g] = first;
+        sMask[g] = mask;
+        any = mask != 0;
+    }
+    const uint64_t bal = __ballot(any);
+    if (lane == 0) sCnt[wave] = __builtin_popcountll(bal);
+    __syncthreads();
+    int32_t base = 0, ng = 0;
+#pragma unroll
+    for (int w = 0; w < kBpWaves; ++w) {
+        base += w < wave ? sCnt[w] : 0;
+        ng += sCnt[w];
+    }
+    if (any) sGl[base + __builtin_popcountll(bal & ((uint64_t(1) << lane) - 1))] = g;
+    __syncthreads();
+
+    // ---- Lane roles.  A: row (input channel c0 + lane % 32), entry parity
+    // kk.  B: output pixel lane % 32 of the wave's block, output channel 2s + kk.
+    const int col = lane & 31, kk = lane >> 5;
+    const int32_t HWo = a.HWo, HWi = a.H * a.W;
+    const int32_t ybytes = int32_t(int64_t(a.npix / HWo) * a.n * HWo * 4);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(ybytes), kRawBufferFlags);
+    const uint32_t chb = uint32_t(HWo) * 4;   // bytes between dY channels
+    const int32_t p = p0 + wave * 32 + col;
+    uint32_t yk = kBufferOutOfRange;          // byte offset of the pixel's dY value at channel kk
+    int64_t xo = -1;                          // element offset of its dX value at channel 0
+    int32_t ih0 = 0, iw0 = 0;                 // the input position it reads (oh * sh, ow * sw)
+    if (p < a.npix) {
+        const int32_t b = p / HWo, hw = p - b * HWo;
+        const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+        ih0 = oh * a.sh;
+        iw0 = ow * a.sw;
+        yk = uint32_t((int64_t(b) * a.n * HWo + hw) * 4) + uint32_t(kk) * chb;
+        xo = int64_t(b) * a.m * HWi + int64_t(ih0) * a.W + iw0;
+    }
+    auto load_b = [&](float (&bv)[S], int32_t gg) __attribute__((always_inline)) {
+        const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
+        const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                rY, int32_t(2 * s < lim ? yk : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+    };
+    // Stage of col-groups sGl[j0 .. j0 + CG): row c holds, for slot j, the
+    // D row of the block where col-group sGl[j0 + j] keeps channel c0 + c
+    // (zeros if it does not, or past the last col-group).  Copy u of a row
+    // covers floats 64u .. 64u + 63: slot (64u + lane) / N, entry lane % N.
+    const v4i32 rD = buffer_rsrc(a.D, int32_t(int64_t(a.t) * N * 4));
+    auto copy_a = [&](int32_t j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < CPR; ++u) {
+            const int32_t j = j0 + (64 * u + lane) / N;
+            const int32_t gg = j < ng ? sGl[j] : 0;
+            const int32_t first = sFirst[gg];
+            const uint32_t mask = j < ng ? sMask[gg] : 0u;
+#pragma unroll
+            for (int rr = 0; rr < 32 / kBpWaves; ++rr) {
+                const int32_t row = wave * (32 / kBpWaves) + rr;
+                const bool kept = (mask >> row) & 1;
+                const int32_t z = first + __builtin_popcount(mask & ((1u << row) - 1));
+                copy4_to_lds(rD, (const lds_char*)(sA + row * AP + 64 * u),
+                             kept ? (z * N + (lane % N)) * 4 : int32_t(kBufferOutOfRange), 0);
+            }
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    auto multiply = [&](int slot, const float (&bv)[S]) __attribute__((always_inline)) {
+        const float* ar = &sA[col * AP + slot * N + kk];
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc = M::step(ar[2 * s], bv[s], acc);
+    };
+
+    if (ng > 0) {
+        float b0[S], b1[S];
+        copy_a(0);
+        load_b(b0, sGl[0]);
+        vm_wait<0>();
+        __syncthreads();
+        // Col-group j multiplies register set j % 2 (CG is even) and loads
+        // col-group j + 1's dY values into the other one.
+        for (int32_t j0 = 0; j0 < ng; j0 += CG) {
+            static_for<CG>([&](auto J) {
+                constexpr int jj = decltype(J)::value;
+                float (&cur)[S] = (jj & 1) ? b1 : b0;
+                float (&nxt)[S] = (jj & 1) ? b0 : b1;
+                if (j0 + jj < ng) {
+                    if (j0 + jj + 1 < ng) load_b(nxt, sGl[j0 + jj + 1]);
+                    multiply(jj, cur);
+                }
+            });
+            if (j0 + CG < ng) {
+                __syncthreads();   // every wave is done with the stage
+                copy_a(j0 + CG);
+                vm_wait<0>();
+                __syncthreads();
+            }
+        }
+    }
+
+    // ---- Store: MFMA (row, col) -> dX channel c0 + row at the lane's input
+    // position; a strided layer's other positions of the sh x sw block get 0
+    // (the blocks of all output pixels cover the input once: Ho * sh >= H).
+    if (xo >= 0) {
+        const int32_t dhe = min(a.sh, a.H - ih0), dwe = min(a.sw, a.W - iw0);
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) {
+            const int32_t c = c0 + M::row(lane, r);
+            if (c >= a.m) continue;
+            float* q = &dx[xo + int64_t(c) * HWi];
+            store_out(q, acc[r]);
+            if (a.sh * a.sw > 1)
+                for (int32_t dh = 0; dh < dhe; ++dh)
+                    for (int32_t dw = 0; dw < dwe; ++dw)
+                        if (dh != 0 || dw != 0) store_out(q + int64_t(dh) * a.W + dw, 0.f);
+        }
+    }
+}
+
 }  // namespace
 
 bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
@@ -493,7 +459,7 @@ bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, i
     const bool pw = a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0;                       // any stride
     const bool k3 = a.kh == 3 && a.kw == 3 && a.sh == a.sw && (a.sh == 1 || a.sh == 2);   // any padding
     if (!pw && !k3) return false;
-    if (k3 && int64_t(a.t) * a.N * 9 * 4 >= (int64_t(1) << 31)) return false;   // D through a buffer
+    if (int64_t(a.t) * a.N * a.KK * 4 >= (int64_t(1) << 31)) return false;   // D through a buffer
     if (a.G > kBpMaxG) return false;
     if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31)) return false;   // 32-bit buffer offsets
     return true;
