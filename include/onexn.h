@@ -280,9 +280,12 @@ onexn_status onexn_fc_fwd(const int32_t* P_dev, const int32_t* I_dev, const void
  *   "kernel"      1: generic gather kernels for every layer
  *   "pw_kernel"   1x1 fp32 N = 16/32: 1 resident tile, 3 register operands
  *   "pwb_kernel"  1x1 bf16 N = 32: 1 register-gathered, 2 LDS-staged
+ *   "bwd_kernel"  backward: 1 general kernels for every layer, 2 the stride-2
+ *                 3x3 input gradient with all nine taps per pixel (instead of
+ *                 one launch per parity class of input pixels)
  *   "pw_wgs", "pwb_gp", "pwb_rp", "pwb_wgs", "direct_kdb", "direct_tile",
  *   "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "kxkf_split",
- *   "nhwc_tile", "bwd_kernel", "bwd_split":
+ *   "nhwc_tile", "bwd_split":
  *                 tile shapes, workgroup counts and pipeline depths of the
  *                 kernel families (a value the family cannot use falls back to
  *                 its default, or makes the conv call fail with UNSUPPORTED).

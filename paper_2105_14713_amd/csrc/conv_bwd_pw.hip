@@ -451,6 +451,190 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Input gradient of a stride-2 3x3 layer by parity class.  An input pixel
+// (ih, iw) receives tap (q, r) only where ih + ph - q and iw + pw - r are
+// even, so the pixels with one parity of (ih + ph, iw + pw) share their taps:
+// (even, even) taps q, r in {0, 2} (four), mixed ones two, (odd, odd) the
+// centre tap only.  One launch per class (QA, RB = the parities of the taps
+// it takes) walks that class's pixels densely (iw = 2j + bb for consecutive
+// j: consecutive lanes read consecutive dY columns) and multiplies only its
+// taps, where the single 3x3 kernel multiplies all nine and reads zeros for
+// the rest.  Steps are (col-group, tap) pairs, eight per stage: the stage's
+// 32 x N tiles (D rows of the kept channels at the tap, gathered from D's
+// [block][row][tap] order) are copied into LDS between two barriers as in
+// the 1x1 kernel; dY values are loaded one step ahead.
+// ---------------------------------------------------------------------------
+
+template <int N, int QA, int RB>
+__global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu(4))) bwd_data_s2(ConvArgs a, const float* __restrict__ dy,
+                                                           float* __restrict__ dx, int32_t ca, int32_t cb) {
+    typedef PwMfma<32> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int NQ = QA == 0 ? 2 : 1, NR = RB == 0 ? 2 : 1;
+    constexpr int NT = NQ * NR;                         // taps of the class
+    constexpr int CG = 8 / NT;                          // col-groups per stage
+    constexpr int STEPS = CG * NT;                      // (col-group, tap) steps per stage: 8
+    constexpr int S = N / 2;                            // MFMA steps per (col-group, tap)
+    constexpr int RW = STEPS * N;                       // floats of a staged row
+    constexpr int AP = RW + 1;                          // LDS pitch of a staged row
+    constexpr int CPR = RW / 64;                        // 64-float copies per row
+    static_assert(RW % 64 == 0 && 32 % kBpWaves == 0, "whole copies, rows split over waves");
+    __shared__ int32_t sFirst[kBpMaxG];
+    __shared__ uint32_t sMask[kBpMaxG];
+    __shared__ int32_t sGl[kBpMaxG];
+    __shared__ int32_t sCnt[kBpWaves];
+    __shared__ float sA[32 * AP];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t c0 = int32_t(blockIdx.y) * 32;
+    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first pixel of the class
+
+    // ---- Index prologue (as in the 3x3 kernel).
+    const int32_t g = tid;
+    bool any = false;
+    const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.I), 0, __builtin_amdgcn_readfirstlane(a.t * 4), kRawBufferFlags);
+    if (g < a.G) {
+        int32_t zb, ze;
+        group_range(a, g, zb, ze);
+        const int32_t first = run_first(rI, zb, ze, c0);
+        uint32_t mask = 0;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int32_t e = first + k;
+            const int32_t c = e < ze ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)) : INT32_MAX;
+            if (c < c0 + 32 && c < a.m) mask |= 1u << (c - c0);
+        }
+        sFirst[g] = first;
+        sMask[g] = mask;
+        any = mask != 0;
+    }
+    const uint64_t bal = __ballot(any);
+    if (lane == 0) sCnt[wave] = __builtin_popcountll(bal);
+    __syncthreads();
+    int32_t base = 0, ng = 0;
+#pragma unroll
+    for (int w = 0; w < kBpWaves; ++w) {
+        base += w < wave ? sCnt[w] : 0;
+        ng += sCnt[w];
+    }
+    if (any) sGl[base + __builtin_popcountll(bal & ((uint64_t(1) << lane) - 1))] = g;
+    __syncthreads();
+
+    // ---- Lane roles as in the 3x3 kernel; the lane's pixel is pixel p of
+    // the class: (b, i, j) -> (ih, iw) = (2i + ca, 2j + cb).
+    const int col = lane & 31, kk = lane >> 5;
+    const int32_t HWo = a.HWo, HWi = a.H * a.W;
+    const int32_t batch = a.npix / HWo;
+    const int32_t hc = (a.H - ca + 1) / 2, wc = (a.W - cb + 1) / 2;   // the class's rows and columns
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
+        kRawBufferFlags);
+    const uint32_t chb = uint32_t(HWo) * 4;
+    const int32_t p = p0 + wave * 32 + col;
+    int64_t xo = -1;
+    uint32_t yk[NT];                          // per class tap: byte offset of dY at channel kk (or out of range)
+    {
+        const bool in = p < batch * hc * wc;
+        const int32_t b = in ? p / (hc * wc) : 0, rem = p - b * hc * wc;
+        const int32_t i = rem / wc, j = rem - i * wc;
+        const int32_t ih = 2 * i + ca, iw = 2 * j + cb;
+        if (in) xo = int64_t(b) * a.m * HWi + int64_t(ih) * a.W + iw;
+        const int64_t ybase = int64_t(b) * a.n * HWo;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int32_t q = QA + 2 * (t / NR), r = RB + 2 * (t % NR);
+            const int32_t oh = (ih + a.ph - q) >> 1, ow = (iw + a.pw - r) >> 1;   // exact: the class's parity
+            const bool ok = in && ih + a.ph - q >= 0 && iw + a.pw - r >= 0 && oh < a.Ho && ow < a.Wo;
+            yk[t] = ok ? uint32_t((ybase + int64_t(oh) * a.Wo + ow) * 4) + uint32_t(kk) * chb : kBufferOutOfRange;
+        }
+    }
+    auto load_b = [&](float (&bv)[S], int32_t gg, int t) __attribute__((always_inline)) {
+        const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
+        const int32_t lim = a.n - ob - kk;
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                rY, int32_t(2 * s < lim ? yk[t] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+    };
+    // Stage of col-groups sGl[j0 .. j0 + CG): row c, step k = slot * NT + t,
+    // entry i holds D[z][i][tap t] for the block z where col-group
+    // sGl[j0 + slot] keeps channel c0 + c (zero if none).  Copy u of a row
+    // covers floats 64u .. 64u + 63.
+    const v4i32 rD = buffer_rsrc(a.D, int32_t(int64_t(a.t) * N * 9 * 4));
+    auto copy_a = [&](int32_t j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < CPR; ++u) {
+            const int32_t f = 64 * u + lane, step = f / N, i = f % N;
+            const int32_t slot = step / NT, t = step % NT;
+            const int32_t tap = (QA + 2 * (t / NR)) * 3 + RB + 2 * (t % NR);
+            const int32_t jj = j0 + slot;
+            const int32_t gg = jj < ng ? sGl[jj] : 0;
+            const int32_t first = sFirst[gg];
+            const uint32_t mask = jj < ng ? sMask[gg] : 0u;
+#pragma unroll
+            for (int rr = 0; rr < 32 / kBpWaves; ++rr) {
+                const int32_t row = wave * (32 / kBpWaves) + rr;
+                const bool kept = (mask >> row) & 1;
+                const int32_t z = first + __builtin_popcount(mask & ((1u << row) - 1));
+                copy4_to_lds(rD, (const lds_char*)(sA + row * AP + 64 * u),
+                             kept ? ((z * N + i) * 9 + tap) * 4 : int32_t(kBufferOutOfRange), 0);
+            }
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    auto multiply = [&](int step, const float (&bv)[S]) __attribute__((always_inline)) {
+        const float* ar = &sA[col * AP + step * N + kk];
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc = M::step(ar[2 * s], bv[s], acc);
+    };
+
+    if (ng > 0) {
+        float b0[S], b1[S];
+        copy_a(0);
+        load_b(b0, sGl[0], 0);
+        vm_wait<0>();
+        __syncthreads();
+        // Step k of a stage (slot k / NT, tap k % NT) multiplies register set
+        // k % 2 (eight steps per stage) and loads step k + 1's dY values.
+        for (int32_t j0 = 0; j0 < ng; j0 += CG) {
+            static_for<STEPS>([&](auto K) {
+                constexpr int k = decltype(K)::value;
+                constexpr int slot = k / NT, t = k % NT;
+                float (&cur)[S] = (k & 1) ? b1 : b0;
+                float (&nxt)[S] = (k & 1) ? b0 : b1;
+                if (j0 + slot < ng) {
+                    if (t + 1 < NT)
+                        load_b(nxt, sGl[j0 + slot], t + 1 < NT ? t + 1 : 0);
+                    else if (j0 + slot + 1 < ng)
+                        load_b(nxt, sGl[j0 + slot + 1], 0);
+                    multiply(k, cur);
+                }
+            });
+            if (j0 + CG < ng) {
+                __syncthreads();
+                copy_a(j0 + CG);
+                vm_wait<0>();
+                __syncthreads();
+            }
+        }
+    }
+
+    if (xo >= 0) {
+#pragma unroll
+        for (int r = 0; r < M::ACC; ++r) {
+            const int32_t c = c0 + M::row(lane, r);
+            if (c < a.m) store_out(&dx[xo + int64_t(c) * HWi], acc[r]);
+        }
+    }
+}
+
 }  // namespace
 
 bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
@@ -486,11 +670,36 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
             hipLaunchKernelGGL((bwd_data_k3<32, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
         else
             hipLaunchKernelGGL((bwd_data_k3<16, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
-    } else {
+    } else if (tuning(kTuneBwdKernel) == 2) {   // all nine taps for every pixel
         if (a.N == 32)
             hipLaunchKernelGGL((bwd_data_k3<32, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
         else
             hipLaunchKernelGGL((bwd_data_k3<16, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
+    } else {
+        // One launch per parity class: pixels (2i + ca, 2j + cb) take the taps
+        // of parities ((ca + ph) % 2, (cb + pw) % 2).
+        const int32_t batch = a.npix / a.HWo;
+        for (int32_t ca = 0; ca < 2 && ca < a.H; ++ca)
+            for (int32_t cb = 0; cb < 2 && cb < a.W; ++cb) {
+                const int64_t cpix = int64_t(batch) * ((a.H - ca + 1) / 2) * ((a.W - cb + 1) / 2);
+                const dim3 cgrid{uint32_t((cpix + kBpPix - 1) / kBpPix), uint32_t(ctiles), 1};
+                const int cls = ((ca + a.ph) & 1) << 1 | ((cb + a.pw) & 1);
+                auto go = [&](auto k32, auto k16) {
+                    if (a.N == 32)
+                        hipLaunchKernelGGL(k32, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
+                    else
+                        hipLaunchKernelGGL(k16, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
+                };
+                switch (cls) {
+                    case 0: go(bwd_data_s2<32, 0, 0>, bwd_data_s2<16, 0, 0>); break;
+                    case 1: go(bwd_data_s2<32, 0, 1>, bwd_data_s2<16, 0, 1>); break;
+                    case 2: go(bwd_data_s2<32, 1, 0>, bwd_data_s2<16, 1, 0>); break;
+                    default: go(bwd_data_s2<32, 1, 1>, bwd_data_s2<16, 1, 1>); break;
+                }
+                const hipError_t cerr = hipGetLastError();
+                if (cerr != hipSuccess)
+                    return fail(ONEXN_ERR_HIP, "conv2d_bwd_data: launch failed: %s", hipGetErrorString(cerr));
+            }
     }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_data: launch failed: %s", hipGetErrorString(err));

@@ -148,17 +148,20 @@ def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
     np.testing.assert_array_equal(dD, ref_dD)
 
 
-@pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "general"])
-@pytest.mark.parametrize("geom", [(3, 1, 1), (3, 2, 1), (7, 2, 3)], ids=["3x3s1", "3x3s2", "7x7s2"])
+@pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "general", "nine_taps"])
+@pytest.mark.parametrize("geom", [(3, 1, 1), (3, 2, 1), (3, 2, 0), (7, 2, 3)], ids=["3x3s1", "3x3s2", "3x3s2p0", "7x7s2"])
 @pytest.mark.parametrize("N", [16, 32])
 def test_bwd_kxk_kernels_agree_with_oracle(kernel, geom, N, tune):
-    """The k x k weight gradient through the matrix-core kernel (taps as a grid
-    dimension, padding read as zeros; one pixel range per item and three) and
-    through the general one: fp32 random 72 -> 40 at 13x11 within 1e-5, and
-    integer data exactly."""
+    """The k x k gradients through the matrix-core kernels (weight gradient
+    over (block, tap) pair tiles with one pixel range per tile and with three;
+    stride-2 3x3 input gradient by parity class, and with all nine taps per
+    pixel: bwd_kernel = 2) and through the general ones: fp32 random 72 -> 40
+    at 13x11 within 1e-5, and integer data exactly."""
     k, s, pd = geom
     if kernel == "general":
         tune("bwd_kernel", 1)
+    if kernel == "nine_taps":
+        tune("bwd_kernel", 2)
     if kernel == "matrix_split3":
         tune("bwd_split", 3)
     gen = torch.Generator().manual_seed(31 + N + k)
