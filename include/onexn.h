@@ -282,7 +282,9 @@ onexn_status onexn_fc_fwd(const int32_t* P_dev, const int32_t* I_dev, const void
  *   "pwb_kernel"  1x1 bf16 N = 32: 1 register-gathered, 2 LDS-staged
  *   "bwd_kernel"  backward: 1 general kernels for every layer, 2 the stride-2
  *                 3x3 input gradient with all nine taps per pixel (instead of
- *                 one launch per parity class of input pixels)
+ *                 one launch per parity class of input pixels), 3 the 1x1
+ *                 weight gradient staged one pixel per access (instead of
+ *                 16-byte pixel quads)
  *   "pw_wgs", "pwb_gp", "pwb_rp", "pwb_wgs", "direct_kdb", "direct_tile",
  *   "fma_tpw", "fma_no_v4", "fma_tile", "kxk_split", "kxk_tp", "kxkf_split",
  *   "nhwc_tile", "bwd_split":

@@ -893,6 +893,136 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
     }
 }
 
+
+// 1x1 stride-1 unpadded layers whose images hold a multiple of 4 pixels: the
+// same work items, with the chunk staged four pixels at a time.  A thread
+// loads a 16-byte quad of pixels of RPT rows of each operand (one
+// buffer_load_dwordx4 per row, a quad never crossing an image) and writes it
+// with one 16-byte LDS store; rows sit at a 16-byte-aligned pitch.  An MFMA
+// step's pixel k of lane group k is pixel k * 32/KS + s of the wave's 32, so
+// a lane reads its row's 32/KS consecutive pixels with 16-byte LDS reads.
+// Against one pixel per thread and access: a quarter of the loads, LDS
+// stores and LDS reads per MFMA.
+constexpr int kBqPitch = kBwCh + 4;            // LDS row pitch (floats): rows 16-byte aligned
+
+template <int N>
+__global__ void __launch_bounds__(kBwThreads) bwd_weight_q4(ConvArgs a, const float* __restrict__ x,
+                                                             const float* __restrict__ dy,
+                                                             float* __restrict__ dD, int32_t tiles_per_g,
+                                                             int32_t nsplit) {
+    typedef PwMfma<N> M;
+    typedef typename M::acc_t acc_t;
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int KS = M::KS;                  // lane groups = pixels per MFMA step
+    constexpr int P = kBqPitch;
+    constexpr int QPR = kBwCh / 4;             // pixel quads per chunk row
+    constexpr int RG = kBwThreads / QPR;       // row groups
+    constexpr int RPT = N / RG;                // rows per thread and operand
+    constexpr int PPL = 32 / KS;               // consecutive pixels a lane reads per chunk
+    static_assert(kBwThreads % QPR == 0 && N % RG == 0 && PPL % 4 == 0, "quad staging");
+    __shared__ __attribute__((aligned(16))) float sX[N * P];
+    __shared__ __attribute__((aligned(16))) float sY[N * P];
+    __shared__ float sR[kBwWaves][64 * M::ACC];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t item = blockIdx.x;
+    const int32_t split = item % nsplit;
+    const int32_t gt = item / nsplit;
+    const int32_t g = gt / tiles_per_g, tile = gt - g * tiles_per_g;
+    int32_t zb, ze;
+    group_range(a, g, zb, ze);
+    const int32_t e0 = zb + tile * N;          // first block of the tile (one tap)
+    if (e0 >= ze) return;
+    // Pixel range, cut at multiples of 4 (npix is one).
+    const int32_t pb = int32_t(int64_t(a.npix) * split / nsplit) & ~3;
+    const int32_t pe = split + 1 == nsplit ? a.npix : int32_t(int64_t(a.npix) * (split + 1) / nsplit) & ~3;
+
+    const int pq = tid % QPR, rg = tid / QPR;  // this thread's quad and row group
+    const int32_t HWo = a.HWo;
+    const int32_t batch = a.npix / HWo;
+    const uint32_t chb = uint32_t(HWo) * 4;    // channel stride of both X and dY (stride 1, no padding)
+    const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HWo * 4)),
+        kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
+        kRawBufferFlags);
+    uint32_t xr[RPT], yr[RPT];                 // row offsets (bytes), or out of range
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+        const int32_t r = rg + RG * j;
+        const int32_t e = e0 + r;
+        const int32_t c = e < ze ? a.I[e] : -1;
+        xr[j] = uint32_t(c) < uint32_t(a.m) ? uint32_t(c) * chb : kBufferOutOfRange;
+        const int32_t o = g * N + r;
+        yr[j] = o < a.n ? uint32_t(o) * chb : kBufferOutOfRange;
+    }
+    f32x4 vx[RPT], vy[RPT];
+    auto load = [&](int32_t p0) __attribute__((always_inline)) {
+        const int32_t p = p0 + 4 * pq;
+        const bool in = p < pe;
+        const int32_t b = in ? p / HWo : 0, hw = p - b * HWo;
+        const uint32_t bx = uint32_t((int64_t(b) * a.m * HWo + hw) * 4);
+        const uint32_t by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const bool okx = in && xr[j] != kBufferOutOfRange, oky = in && yr[j] != kBufferOutOfRange;
+            vx[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                rX, int32_t(okx ? bx + xr[j] : kBufferOutOfRange), 0, 0));
+            vy[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                rY, int32_t(oky ? by + yr[j] : kBufferOutOfRange), 0, 0));
+        }
+    };
+    auto put = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            *reinterpret_cast<f32x4*>(&sX[(rg + RG * j) * P + 4 * pq]) = vx[j];
+            *reinterpret_cast<f32x4*>(&sY[(rg + RG * j) * P + 4 * pq]) = vy[j];
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    const int rc = lane % N, k = lane / N;
+    const float* ax = sX + rc * P + wave * 32 + k * PPL;
+    const float* ay = sY + rc * P + wave * 32 + k * PPL;
+
+    if (pb < pe) {
+        load(pb);
+        for (int32_t p0 = pb; p0 < pe; p0 += kBwCh) {
+            __syncthreads();   // the previous chunk's reads are done
+            put();
+            __syncthreads();
+            if (p0 + kBwCh < pe) load(p0 + kBwCh);
+#pragma unroll
+            for (int v = 0; v < PPL / 4; ++v) {
+                const f32x4 av = *reinterpret_cast<const f32x4*>(ax + 4 * v);
+                const f32x4 bv = *reinterpret_cast<const f32x4*>(ay + 4 * v);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = M::step(av[e], bv[e], acc);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) sR[wave][r * 64 + lane] = acc[r];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r)
+        acc[r] = ((sR[0][r * 64 + lane] + sR[1][r * 64 + lane]) + sR[2][r * 64 + lane]) + sR[3][r * 64 + lane];
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) {
+        const int32_t e = e0 + M::row(lane, r);
+        if (e >= ze) continue;
+        float* dst = dD + int64_t(e) * N + rc;
+        if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
+        else *dst = acc[r];
+    }
+}
+
 }  // namespace
 
 bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
@@ -928,11 +1058,17 @@ onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* 
         hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a, static_cast<const float*>(x),
                            static_cast<const float*>(dy), dD, int32_t(tiles_per_g), int32_t(nsplit));
     };
+    // 1x1 stride-1 unpadded layers with whole pixel quads per image: quads.
+    const bool quads = a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0 && a.HWo % 4 == 0 &&
+                       (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                       tuning(kTuneBwdKernel) != 3;
     if (a.N == 32) {
-        if (a.KK > 1) go(bwd_weight_pw<32, true>);
+        if (quads) go(bwd_weight_q4<32>);
+        else if (a.KK > 1) go(bwd_weight_pw<32, true>);
         else go(bwd_weight_pw<32, false>);
     } else {
-        if (a.KK > 1) go(bwd_weight_pw<16, true>);
+        if (quads) go(bwd_weight_q4<16>);
+        else if (a.KK > 1) go(bwd_weight_pw<16, true>);
         else go(bwd_weight_pw<16, false>);
     }
     const hipError_t err = hipGetLastError();

@@ -50,6 +50,8 @@ CASES = [  # (n, m, k, stride, pad, B, H, W, N)
     (40, 70, 1, 1, 0, 2, 10, 10, 16),   # three channel tiles, the last partial
     (96, 300, 1, 1, 0, 1, 9, 9, 32),    # col-groups of up to 300 blocks (narrowing rounds)
     (48, 1100, 1, 1, 0, 1, 5, 4, 16),   # col-groups longer than 1024 blocks
+    (72, 40, 1, 1, 0, 3, 8, 6, 32),     # 48-pixel images: the weight gradient staged in pixel quads
+    (40, 33, 1, 1, 0, 2, 4, 5, 16),
     # 1x1 strided at N = 16 / 32: the matrix-core kernel, zeros off the stride grid
     (80, 45, 1, 2, 0, 2, 9, 11, 32),    # odd map: the last block row/column clipped
     (40, 70, 1, 3, 0, 1, 10, 8, 16),
@@ -123,16 +125,19 @@ def test_bwd_resnet50_layer_shape_and_reproducibility():
     np.testing.assert_array_equal(dD, dD2)
 
 
-@pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "general"])
+@pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "no_quads", "no_quads_split3", "general"])
 @pytest.mark.parametrize("N", [16, 32])
 def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
     """The 1x1 gradients through the matrix-core kernels (the weight gradient
-    with one pixel range per tile, and with three whose sums are added) and
-    through the general ones (bwd_kernel = 1): fp32 random, 300 -> 256, and
-    integer data exactly."""
+    with one pixel range per tile, and with three whose sums are added; staged
+    in pixel quads where the 132-pixel images allow, and one pixel per access
+    with bwd_kernel = 3) and through the general ones (bwd_kernel = 1): fp32
+    random, 300 -> 256, and integer data exactly."""
     if kernel == "general":
         tune("bwd_kernel", 1)
-    if kernel == "matrix_split3":
+    if kernel.startswith("no_quads"):
+        tune("bwd_kernel", 3)
+    if kernel.endswith("split3"):
         tune("bwd_split", 3)
     gen = torch.Generator().manual_seed(23 + N)
     w = workloads.gen_weight(gen, 256, 300, 1)
@@ -141,8 +146,8 @@ def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
     dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, 0.5, 1, 0)
     assert rel_err(dx, ref_dx) <= 1e-5
     assert rel_err(dD, ref_dD) <= 1e-5
-    wi, xi = workloads.gen_integer_layer(seed=N, cout=72, cin=50, k=1, batch=3, H=9, W=13, wmax=2, xmax=2)
-    dyi = torch.randint(-2, 3, (3, 72, 9, 13), generator=gen).float()
+    wi, xi = workloads.gen_integer_layer(seed=N, cout=72, cin=50, k=1, batch=3, H=9, W=12, wmax=2, xmax=2)
+    dyi = torch.randint(-2, 3, (3, 72, 9, 12), generator=gen).float()
     dx, dD, ref_dx, ref_dD = _bwd(wi, xi, dyi, N, 0.5, 1, 0)
     np.testing.assert_array_equal(dx, ref_dx)
     np.testing.assert_array_equal(dD, ref_dD)
