@@ -269,9 +269,10 @@ def mask_bench(wl, dev, reps):
 
 def backward_bench(wl, dev, reps):
     """Times one backward pass (onexn_conv2d_bwd_data and onexn_conv2d_bwd_weight
-    on every layer) with HIP events, after checking one layer's gradients
-    against the oracle at sampled entries.  Each of the two gradients does the
-    forward's actual flops (2 * pixels * N * kh * kw * t)."""
+    on every layer) with HIP events, after checking each layer's gradients on
+    the first image against the oracle (every entry of the timed launch's dX
+    there, and of dD over that image alone).  Each of the
+    two gradients does the forward's actual flops (2 * pixels * N * kh * kw * t)."""
     import oracle
     stream = torch.cuda.current_stream(dev)
     rows, t_sum, f_sum, troof = [], 0.0, 0.0, 0.0
@@ -292,29 +293,29 @@ def backward_bench(wl, dev, reps):
             return dx, dD
         dx, dD = run()
         torch.cuda.synchronize()
-        if li == 0:
-            # Parity before timing: sampled dX entries and every dD entry of the
-            # first 8 kept blocks against the oracle on the first image.
-            pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
-            x0, dy0 = x[:1].double().numpy(), dy[:1].double().numpy()
-            ref_dx = oracle.conv2d_bwd_data(dy0, pr.wbar, (layer.H, layer.H), (layer.stride,) * 2,
-                                            (layer.pad,) * 2)
-            dx1 = onexn.conv2d_bwd_data(packed.P, packed.I, packed.D, layer.cout, layer.cin, dyd[:1].contiguous(),
-                                        (layer.H, layer.H), layer.stride, layer.pad)
-            dD1 = onexn.conv2d_bwd_weight(packed.P, packed.I, layer.cout, layer.N, kk, xd[:1].contiguous(),
-                                          dyd[:1].contiguous(), layer.stride, layer.pad)
-            torch.cuda.synchronize()
-            dw = oracle.conv2d_bwd_weight(x0, dy0, pr.T, layer.N, kk, (layer.stride,) * 2, (layer.pad,) * 2)
-            _, _, ref_dD = oracle.pack(dw, pr.T, layer.N)
-            bar = 2e-2 if wl.dtype == "bf16" else 1e-5
+        # Parity before timing, against the oracle on the first image: every
+        # entry of that image's dX from the timed launch (images are
+        # independent), and every dD entry of a launch on that image alone.
+        pr = oracle.prune(w.double().numpy(), layer.N, layer.p, layer.rearrange)
+        x0, dy0 = x[:1].double().numpy(), dy[:1].double().numpy()
+        ref_dx = oracle.conv2d_bwd_data(dy0, pr.wbar, (layer.H, layer.H), (layer.stride,) * 2,
+                                        (layer.pad,) * 2)
+        dx1 = dx[:1]
+        dD1 = onexn.conv2d_bwd_weight(packed.P, packed.I, layer.cout, layer.N, kk, xd[:1].contiguous(),
+                                      dyd[:1].contiguous(), layer.stride, layer.pad)
+        torch.cuda.synchronize()
+        dw = oracle.conv2d_bwd_weight(x0, dy0, pr.T, layer.N, kk, (layer.stride,) * 2, (layer.pad,) * 2)
+        _, _, ref_dD = oracle.pack(dw, pr.T, layer.N)
+        bar = 2e-2 if wl.dtype == "bf16" else 1e-5
 
-            def rel(a, b):
-                return float(abs(a - b).max() / max(abs(b).max(), 1e-300))
-            e1 = rel(dx1.double().cpu().numpy(), ref_dx)
-            e2 = rel(dD1.double().cpu().numpy(), ref_dD)
-            if not (e1 <= bar and e2 <= bar):
-                print(json.dumps({"parity": "FAIL", "layer": layer.name, "dx": e1, "dD": e2}), flush=True)
-                sys.exit(3)
+        def rel(a, b):
+            return float(abs(a - b).max() / max(abs(b).max(), 1e-300))
+        e1 = rel(dx1.double().cpu().numpy(), ref_dx)
+        e2 = rel(dD1.double().cpu().numpy(), ref_dD)
+        if not (e1 <= bar and e2 <= bar):
+            print(json.dumps({"parity": "FAIL", "layer": layer.name, "dx": e1, "dD": e2}), flush=True)
+            sys.exit(3)
+        errs = {"dx_rel_err": float(f"{e1:.3g}"), "dD_rel_err": float(f"{e2:.3g}")}
         for _ in range(2):
             run()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -326,7 +327,7 @@ def backward_bench(wl, dev, reps):
         tl = e0.elapsed_time(e1) / reps / 1e3
         fa = 2.0 * 2.0 * layer.out_pixels(wl.batch) * layer.N * layer.k * layer.k * packed.t
         rows.append({"layer": layer.name, "us": round(tl * 1e6, 1), "gflop": round(fa / 1e9, 3),
-                     "tflops": round(fa / tl / 1e12, 3)})
+                     "tflops": round(fa / tl / 1e12, 3), **errs})
         t_sum, f_sum, troof = t_sum + tl, f_sum + fa, troof + fa / (peak * 1e12)
         del dx, dD, xd, dyd
     print(json.dumps({
