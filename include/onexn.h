@@ -232,7 +232,9 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
  * zeroed dD, so the last bits can vary run to run; setting the tuning
  * "bwd_split" to 1 makes it one range per item (fixed order, slower).  Such
  * a call launches a fill of dD first: a HIP error from its second launch may
- * leave dD zeroed.
+ * leave dD zeroed.  The input gradient of a stride-2 3x3 fp32 layer at
+ * N = 16/32 is four launches, one per parity class of input pixels: a HIP
+ * error from a later one leaves the earlier classes' dx entries written.
  * Arguments, ownership, the int32 size limits and the errors are those of
  * onexn_conv2d_fwd; P, I, D are the forward's BSR arrays.
  */
