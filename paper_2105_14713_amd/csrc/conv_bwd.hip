@@ -23,9 +23,10 @@
 // bwd_data_fewc.  Layers with at most four input channels (a network's first
 // convolution), fp32: every input channel of a pixel in one lane.  The
 // layer's weights (Omega-bar, dense, [tap][output channel][input channel],
-// zero where pruned) are scattered into LDS once per workgroup.  A wave takes
-// 64 input pixels of one row whose columns share their residue modulo the
-// stride (iw = cb + sw * (64k + lane)), so the taps whose stride divides are
+// zero where pruned) are scattered into LDS once per workgroup.  A workgroup
+// takes a contiguous range of (row, residue, column chunk) tasks, the ranges
+// of one XCD consecutive.  A wave takes 64 input pixels of one row whose
+// columns share their residue modulo the stride (iw = cb + sw * (64k + lane)), so the taps whose stride divides are
 // the same for the whole wave and the others are skipped; for each such tap
 // and output channel a lane loads one dY value (consecutive lanes,
 // consecutive output columns; out-of-range positions read zeros) and adds it,
@@ -164,8 +165,14 @@ __global__ void __launch_bounds__(64 * kFcWaves) bwd_data_fewc(ConvArgs a, const
         const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(batch * n * HWo * 4), kRawBufferFlags);
     const uint32_t chb = uint32_t(HWo) * 4;  // bytes between dY channels
     const int32_t per_row = a.sw * cpr;      // wave tasks per input row
-    for (int32_t task = int32_t(blockIdx.x) * kFcWaves + wave; task < tasks;
-         task += int32_t(gridDim.x) * kFcWaves) {
+    // A workgroup takes a contiguous range of tasks (consecutive input rows,
+    // which read overlapping dY rows: a dY row feeds kh consecutive input
+    // rows), and consecutive ranges run on one XCD, so those rows are
+    // fetched into that XCD's L2 once (round-robin tasks: 19 % L2 hits).
+    const int32_t L = xcd_remap(int32_t(blockIdx.x), int32_t(gridDim.x));
+    const int32_t t0 = int32_t(int64_t(tasks) * L / gridDim.x);
+    const int32_t t1 = int32_t(int64_t(tasks) * (L + 1) / gridDim.x);
+    for (int32_t task = t0 + wave; task < t1; task += kFcWaves) {
         const int32_t row = task / per_row, rem = task - row * per_row;
         const int32_t cb = rem / cpr, k = rem - cb * cpr;
         const int32_t b = row / a.H, ih = row - b * a.H;
