@@ -95,6 +95,19 @@ __device__ __forceinline__ int32_t run_first(__amdgpu_buffer_rsrc_t rI, int32_t 
 // once: deterministic.
 // ---------------------------------------------------------------------------
 
+// Workgroup -> (32-channel tile, pixel tile) of the input-gradient kernels: a
+// one-dimensional grid in which the channel tiles of one pixel tile are
+// consecutive logical ids, and consecutive logical ids run on one XCD, so
+// the dY values of a pixel tile are fetched into one L2 (with the pixel
+// tile as the grid's x and the channel tile as its y they were spread over
+// all eight).
+__device__ __forceinline__ void dx_tile(const ConvArgs& a, int32_t& c0, int32_t& p0) {
+    const int32_t ct = (a.m + 31) / 32;
+    const int32_t L = xcd_remap(int32_t(blockIdx.x), int32_t(gridDim.x));
+    c0 = (L % ct) * 32;
+    p0 = (L / ct) * kBpPix;
+}
+
 template <typename F, int... Is>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
     (f(std::integral_constant<int, Is>{}), ...);
@@ -122,8 +135,8 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t c0 = int32_t(blockIdx.y) * 32;
-    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first input pixel
+    int32_t c0, p0;                                     // first input channel and input pixel
+    dx_tile(a, c0, p0);
 
     // ---- Index prologue: thread g < G finds col-group g's run of blocks in
     // [c0, c0 + 32): entries first, first + 1, ... in ascending channel order,
@@ -310,8 +323,8 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t c0 = int32_t(blockIdx.y) * 32;
-    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first output pixel
+    int32_t c0, p0;                                     // first input channel and output pixel
+    dx_tile(a, c0, p0);
 
     // ---- Index prologue (as in the 3x3 kernel).
     const int32_t g = tid;
@@ -489,8 +502,8 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t c0 = int32_t(blockIdx.y) * 32;
-    const int32_t p0 = int32_t(blockIdx.x) * kBpPix;   // first pixel of the class
+    int32_t c0, p0;                                     // first input channel and pixel of the class
+    dx_tile(a, c0, p0);
 
     // ---- Index prologue (as in the 3x3 kernel).
     const int32_t g = tid;
@@ -655,9 +668,9 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
     const int64_t pix = k3 ? int64_t(a.npix / a.HWo) * a.H * a.W : int64_t(a.npix);
     const int64_t ptiles = (pix + kBpPix - 1) / kBpPix;
     const int64_t ctiles = (int64_t(a.m) + 31) / 32;
-    if (ptiles > INT32_MAX || ctiles > 65535)
+    if (ptiles * ctiles > INT32_MAX)
         return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_data: grid out of range");
-    const dim3 grid{uint32_t(ptiles), uint32_t(ctiles), 1};
+    const dim3 grid{uint32_t(ptiles * ctiles), 1, 1};
     const float* y = static_cast<const float*>(dy);
     float* x = static_cast<float*>(dx);
     if (!k3) {
@@ -682,7 +695,7 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
         for (int32_t ca = 0; ca < 2 && ca < a.H; ++ca)
             for (int32_t cb = 0; cb < 2 && cb < a.W; ++cb) {
                 const int64_t cpix = int64_t(batch) * ((a.H - ca + 1) / 2) * ((a.W - cb + 1) / 2);
-                const dim3 cgrid{uint32_t((cpix + kBpPix - 1) / kBpPix), uint32_t(ctiles), 1};
+                const dim3 cgrid{uint32_t((cpix + kBpPix - 1) / kBpPix * ctiles), 1, 1};
                 const int cls = ((ca + a.ph) & 1) << 1 | ((cb + a.pw) & 1);
                 auto go = [&](auto k32, auto k16) {
                     if (a.N == 32)
