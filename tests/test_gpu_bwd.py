@@ -125,6 +125,25 @@ def test_bwd_resnet50_layer_shape_and_reproducibility():
     np.testing.assert_array_equal(dD, dD2)
 
 
+@pytest.mark.parametrize("name", ["s2b1_3x3", "s2b1_down", "s3b2_1x1a", "s1b1_1x1b"])
+def test_bwd_resnet50_full_batch(name):
+    """ResNet-50 layers at the backward benchmark's size and launch
+    configuration (batch 64, fp32, N = 32, p = 0.5): the stride-2 3x3 input
+    gradient's parity-class launches and the pair-tiled weight gradient; the
+    strided 1x1 input gradient with its zeroed positions; the 1x1 input
+    gradient with 1024 input channels; the 64 -> 256 layer's quad-staged
+    weight gradient.  Every dX and dD entry against the oracle, within 1e-5
+    of the largest."""
+    layer = [l for l in workloads.resnet50_convs() if l.name == name][0]
+    print(f"bwd full batch {name}", flush=True)
+    w, x = workloads.gen_layer(layer, 64)
+    gen = torch.Generator().manual_seed(layer.seed + 7)
+    dy = torch.randn((64, layer.cout, layer.Ho, layer.Ho), generator=gen)
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, layer.N, layer.p, layer.stride, layer.pad)
+    assert rel_err(dx, ref_dx) <= 1e-5
+    assert rel_err(dD, ref_dD) <= 1e-5
+
+
 @pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "no_quads", "no_quads_split3", "general"])
 @pytest.mark.parametrize("N", [16, 32])
 def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
