@@ -214,11 +214,18 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     // consecutive taps stay in one counted sequence.
     auto load_b = [&](float (&bv)[S], int32_t gg, int tap) __attribute__((always_inline)) {
         const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
-        const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+        if (ob + N <= a.n) {   // (uniform) every row exists: no per-step mask
 #pragma unroll
-        for (int s = 0; s < S; ++s)
-            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                rY, int32_t(2 * s < lim ? yk[tap] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(yk[tap]), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        } else {
+            const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(2 * s < lim ? yk[tap] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        }
     };
     // Tile of col-group gg: row c (channel c0 + c) is D row z (RW floats) if
     // the col-group keeps the channel at block z, else zeros (an out-of-range
@@ -380,11 +387,18 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     }
     auto load_b = [&](float (&bv)[S], int32_t gg) __attribute__((always_inline)) {
         const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
-        const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+        if (ob + N <= a.n) {   // (uniform) every row exists: no per-step mask
 #pragma unroll
-        for (int s = 0; s < S; ++s)
-            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                rY, int32_t(2 * s < lim ? yk : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(yk), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        } else {
+            const int32_t lim = a.n - ob - kk;   // this lane's rows 2s + kk < n - ob
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(2 * s < lim ? yk : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        }
     };
     // Stage of col-groups sGl[j0 .. j0 + CG): row c holds, for slot j, the
     // D row of the block where col-group sGl[j0 + j] keeps channel c0 + c
@@ -567,11 +581,18 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
     }
     auto load_b = [&](float (&bv)[S], int32_t gg, int t) __attribute__((always_inline)) {
         const int32_t ob = __builtin_amdgcn_readfirstlane(gg * N);
-        const int32_t lim = a.n - ob - kk;
+        if (ob + N <= a.n) {   // (uniform) every row exists: no per-step mask
 #pragma unroll
-        for (int s = 0; s < S; ++s)
-            bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                rY, int32_t(2 * s < lim ? yk[t] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(yk[t]), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        } else {
+            const int32_t lim = a.n - ob - kk;
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                bv[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    rY, int32_t(2 * s < lim ? yk[t] : kBufferOutOfRange), int32_t(uint32_t(ob + 2 * s) * chb), 0));
+        }
     };
     // Stage of col-groups sGl[j0 .. j0 + CG): row c, step k = slot * NT + t,
     // entry i holds D[z][i][tap t] for the block z where col-group
