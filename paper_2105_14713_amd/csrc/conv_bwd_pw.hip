@@ -744,7 +744,7 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
 
 // ---------------------------------------------------------------------------
 // Weight gradient of the kept blocks on matrix cores: fp32, NCHW, N in
-// {16, 32}, any kernel size, stride and padding.
+// {16, 32}, kernels of up to 63 taps, any stride and padding.
 //
 //     dD[z][i][q][r] = sum over output pixels of
 //                      X[I[z]][oh*sh - ph + q][ow*sw - pw + r] * dY[gN + i][oh][ow]
@@ -826,7 +826,7 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
     // the col-group's output channel (bytes); a pair past the col-group's, a
     // channel outside [0, m) or a row past n reads zeros.
     uint32_t xr[RPT], yr[RPT];
-    int32_t tq[RPT];                           // tap row q << 8 | tap column r, or -1
+    int32_t tq[RPT];                           // row's tap index (KT), 63 for no pair
     uint32_t valid = 0;                        // bit j: row j is a pair with a channel in [0, m)
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
@@ -835,16 +835,17 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
         const int32_t tap = pr < npairs ? pr / cnt : 0;
         const int32_t c = pr < npairs ? a.I[zb + pr - tap * cnt] : -1;
         const bool ok = uint32_t(c) < uint32_t(a.m);
-        xr[j] = ok ? uint32_t(c) * xchb : 0u;
-        tq[j] = ok ? (tap / a.kw) << 8 | (tap % a.kw) : -1;
+        // (KT: the channel's byte offset plus the tap's shift (q*W + r)*4.)
+        const int32_t q = tap / a.kw;
+        xr[j] = ok ? uint32_t(c) * xchb + (KT ? uint32_t(q * a.W + tap - q * a.kw) * 4 : 0u) : 0u;
+        tq[j] = ok ? tap : 63;
         valid |= uint32_t(ok) << j;
         const int32_t o = g * N + r;
         yr[j] = o < a.n ? uint32_t(o) * chb : kBufferOutOfRange;
     }
     // A 1x1 layer (KT false) has the one tap (0, 0): one bounds check per
-    // pixel.  Otherwise each row checks its own shift (a version that took a
-    // one-check path for tiles within one tap needed 188 registers, against
-    // 148).
+    // pixel.  Otherwise the pixel's taps that land inside the image form a
+    // bit mask (kh + kw compares), and a row tests its tap's bit.
     float vx[RPT], vy[RPT];
     auto load = [&](int32_t p0) __attribute__((always_inline)) {
         const int32_t p = p0 + px;
@@ -866,14 +867,17 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_pw(ConvArgs a, const fl
                 vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
             }
         } else {
+            // Bit q*kw + r: tap (q, r) reads inside the image (kh * kw <= 63).
+            uint64_t cm = 0, mask = 0;
+            for (int32_t r = 0; r < a.kw; ++r) cm |= uint64_t(uint32_t(iw0 + r) < uint32_t(a.W)) << r;
+            for (int32_t q = 0; q < a.kh; ++q)
+                mask |= uint32_t(ih0 + q) < uint32_t(a.H) ? cm << (q * a.kw) : 0;
+            mask = in ? mask : 0;
 #pragma unroll
             for (int j = 0; j < RPT; ++j) {
-                const int32_t q = tq[j] >> 8, r = tq[j] & 0xff;
-                const bool ok = in && tq[j] >= 0 && uint32_t(ih0 + q) < uint32_t(a.H) &&
-                                uint32_t(iw0 + r) < uint32_t(a.W);
-                const uint32_t xo = bx + xr[j] + uint32_t(q * a.W + r) * 4;
+                const bool ok = (mask >> tq[j]) & 1;
                 vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                    rX, int32_t(ok ? xo : kBufferOutOfRange), 0, 0));
+                    rX, int32_t(ok ? bx + xr[j] : kBufferOutOfRange), 0, 0));
                 vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, int32_t(by + yr[j]), 0, 0));
             }
         }
@@ -1062,6 +1066,7 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_q4(ConvArgs a, const fl
 bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
     if (xdt != ONEXN_F32) return false;
     if (a.N != 16 && a.N != 32) return false;
+    if (a.KK > 63) return false;   // one bit per tap, 63 meaning "no pair"
     if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31) ||
         int64_t(batch) * a.m * a.H * a.W * 4 >= (int64_t(1) << 31))
         return false;   // 32-bit buffer offsets
