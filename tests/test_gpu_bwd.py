@@ -21,12 +21,15 @@ def _gpu():
 
 
 def _bwd(w, x, dy, N, p, s, pd, dx_dtype=None):
-    """(GPU dX, GPU dD, oracle dX, oracle dD) as fp64 numpy; w, x, dy on the host."""
+    """(GPU dX, GPU dD, oracle dX, oracle dD) as fp64 numpy; w, x, dy on the host.
+    Both outputs start as NaN, so an entry a kernel leaves unwritten fails."""
     n, m, k, _ = w.shape
-    H, W = x.shape[2], x.shape[3]
+    B, H, W = x.shape[0], x.shape[2], x.shape[3]
     layer = onexn.prepare_layer(w, N, p, True)
-    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, n, m, dy.cuda(), (H, W), s, pd, dx_dtype)
-    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, n, N, (k, k), x.cuda(), dy.cuda(), s, pd)
+    dxo = torch.full((B, m, H, W), float("nan"), dtype=dx_dtype or dy.dtype, device="cuda")
+    dDo = torch.full((layer.t, N, k, k), float("nan"), dtype=torch.float32, device="cuda")
+    dx = onexn.conv2d_bwd_data(layer.P, layer.I, layer.D, n, m, dy.cuda(), (H, W), s, pd, dx_dtype, out=dxo)
+    dD = onexn.conv2d_bwd_weight(layer.P, layer.I, n, N, (k, k), x.cuda(), dy.cuda(), s, pd, out=dDo)
     torch.cuda.synchronize()
     pr = oracle.prune(w.double().numpy(), N, p, True)
     assert layer.t == pr.t
