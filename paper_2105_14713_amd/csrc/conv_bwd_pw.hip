@@ -1,5 +1,6 @@
-// Input gradient of 1x1 (any stride, no padding) and 3x3 (stride 1 or 2)
-// 1xN-pruned convolutions on matrix cores: fp32, NCHW, N in {16, 32}.
+// Input gradient of 1x1 (any stride, no padding; N in {2, 4, 8, 16, 32}) and
+// 3x3 (stride 1 or 2; N in {16, 32}) 1xN-pruned convolutions on matrix
+// cores: fp32, NCHW.
 //
 // Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
 // (arXiv 2105.14713), Sec. 3.4 (Eq. 7 with Omega-bar, stored as Eq. 8's BSR)
@@ -23,13 +24,13 @@
 //    round of independent loads per 32x narrowing) and records its first
 //    block and a mask of the channels it keeps: channel c0 + k is block
 //    first + popcount(mask below bit k).
-//  - A.  The 32 x N tiles Wt_g of eight col-groups at a time are copied from
-//    D straight into one LDS buffer between two barriers (rows of channels a
-//    col-group does not keep read zeros through an out-of-range offset), so
-//    no registers hold tiles in flight and a wave multiplies 8 x N/2 steps
-//    per barrier pair (a version with one col-group's tile per barrier,
-//    built in LDS one col-group ahead through registers, was 2-16 % slower
-//    per layer).
+//  - A.  The 32 x N tiles Wt_g of 8 col-groups at a time (N = 16, 32) or
+//    256 / N (N <= 8) are copied from D straight into one LDS buffer between
+//    two barriers (rows of channels a col-group does not keep read zeros
+//    through an out-of-range offset), so no registers hold tiles in flight
+//    and a wave multiplies 4N (N >= 16) or 128 MFMA steps per barrier pair
+//    (a version with one col-group's tile per barrier, built in LDS one
+//    col-group ahead through registers, was 2-16 % slower per layer).
 //  - B.  dY rows gN .. gN+N-1 at the wave's pixels, loaded into registers
 //    one col-group ahead.
 // Every output element is written once, by one lane, after a fixed-order
@@ -46,7 +47,7 @@ namespace {
 constexpr int kBpWaves = 8;
 constexpr int kBpThreads = 64 * kBpWaves;
 constexpr int kBpPix = kBpWaves * 32;                   // pixels per workgroup (a 32-pixel block per wave)
-constexpr int kBpMaxG = 256;                            // col-groups (one prologue thread each)
+constexpr int kBpMaxG = kBpThreads;                     // col-groups (one prologue thread each)
 
 // First entry in [zb, ze) of a col-group whose input channel is >= c0 (ze if
 // none).  I ascends within a col-group, so the entries below c0 form a
@@ -316,12 +317,13 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
                                                             float* __restrict__ dx) {
     typedef PwMfma<32> M;
     typedef typename M::acc_t acc_t;
-    constexpr int CG = 8;                               // col-groups per stage
+    constexpr int CG = N >= 16 ? 8 : 256 / N;           // col-groups per stage (a 32 x 8N or 32 x 256 tile)
     constexpr int S = N / 2;                            // MFMA steps per col-group
     constexpr int RW = CG * N;                          // floats of a staged row
     constexpr int AP = RW + 1;                          // LDS pitch of a staged row
     constexpr int CPR = RW / 64;                        // 64-float copies per row
     static_assert(RW % 64 == 0 && 32 % kBpWaves == 0, "whole copies, rows split over waves");
+    static_assert(N >= 2 && 64 % N == 0, "an MFMA step takes two output channels of one col-group");
     __shared__ int32_t sFirst[kBpMaxG];                 // first block of col-group g in the tile
     __shared__ uint32_t sMask[kBpMaxG];                 // bit k: g keeps channel c0 + k
     __shared__ int32_t sGl[kBpMaxG];                    // col-groups with a kept block in the tile
@@ -673,9 +675,10 @@ __global__ void __launch_bounds__(kBpThreads) __attribute__((amdgpu_waves_per_eu
 
 bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, int32_t batch) {
     if (wdt != ONEXN_F32 || dxdt != ONEXN_F32) return false;
-    if (a.N != 16 && a.N != 32) return false;
-    const bool pw = a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0;                       // any stride
-    const bool k3 = a.kh == 3 && a.kw == 3 && a.sh == a.sw && (a.sh == 1 || a.sh == 2);   // any padding
+    const bool pw = a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0 &&                     // any stride,
+                    (a.N == 2 || a.N == 4 || a.N == 8 || a.N == 16 || a.N == 32);        // N >= 2
+    const bool k3 = a.kh == 3 && a.kw == 3 && a.sh == a.sw && (a.sh == 1 || a.sh == 2) &&   // any padding
+                    (a.N == 16 || a.N == 32);
     if (!pw && !k3) return false;
     if (int64_t(a.t) * a.N * a.KK * 4 >= (int64_t(1) << 31)) return false;   // D through a buffer
     if (a.G > kBpMaxG) return false;
@@ -695,10 +698,13 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
     const float* y = static_cast<const float*>(dy);
     float* x = static_cast<float*>(dx);
     if (!k3) {
-        if (a.N == 32)
-            hipLaunchKernelGGL(bwd_data_pw<32>, grid, dim3(kBpThreads), 0, s, a, y, x);
-        else
-            hipLaunchKernelGGL(bwd_data_pw<16>, grid, dim3(kBpThreads), 0, s, a, y, x);
+        switch (a.N) {
+            case 32: hipLaunchKernelGGL(bwd_data_pw<32>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
+            case 16: hipLaunchKernelGGL(bwd_data_pw<16>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
+            case 8: hipLaunchKernelGGL(bwd_data_pw<8>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
+            case 4: hipLaunchKernelGGL(bwd_data_pw<4>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
+            default: hipLaunchKernelGGL(bwd_data_pw<2>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
+        }
     } else if (a.sh == 1) {
         if (a.N == 32)
             hipLaunchKernelGGL((bwd_data_k3<32, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
@@ -1061,11 +1067,181 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_q4(ConvArgs a, const fl
     }
 }
 
+
+// Weight gradient of 1x1 stride-1 unpadded layers at N <= 8, where an N x N
+// tile would leave the matrix cores mostly idle: the dense product
+//     G[c][o] = sum over pixels of X[c][pixel] * dY[o][pixel]
+// of a tile of 32 input channels and 32 output channels (32/N col-groups)
+// on v_mfma_f32_32x32x2f32, of which only the entries of kept blocks are
+// stored: dD[z][i] = G[I[z]][gN + i] (at p = 0.5 half the tile's work is for
+// pruned blocks).  Items are (channel tile, output-channel tile, pixel
+// range); a prologue finds each of the tile's col-groups' kept blocks among
+// the 32 channels (first block and channel mask, as in the input
+// gradient), and a tile that holds none returns.  Chunks of 128 pixels are
+// staged as in bwd_weight_q4 (Q = 4: 16-byte pixel quads, images of a
+// multiple of 4 pixels) or one pixel per access (Q = 1); four waves split a
+// chunk's pixels and add their sums in wave order.  Each dD entry belongs to
+// one tile: stored once, or added with atomics when pixel ranges split.
+template <int N, int Q>
+__global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const float* __restrict__ x,
+                                                                const float* __restrict__ dy,
+                                                                float* __restrict__ dD, int32_t otiles,
+                                                                int32_t nsplit) {
+    typedef PwMfma<32> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int GPT = 32 / N;                // col-groups per output-channel tile
+    constexpr int P = kBqPitch;
+    constexpr int QPR = kBwCh / Q;             // pixel groups per chunk row
+    constexpr int RG = kBwThreads / QPR;       // row groups
+    constexpr int RPT = 32 / RG;               // rows per thread and operand
+    constexpr int PPL = 16;                    // consecutive pixels a lane reads per chunk
+    typedef typename std::conditional<Q == 4, f32x4, float>::type vq_t;
+    static_assert(N <= 8 && 32 % N == 0 && kBwThreads % QPR == 0 && 32 % RG == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) float sX[32 * P];
+    __shared__ __attribute__((aligned(16))) float sY[32 * P];
+    __shared__ float sR[kBwWaves][64 * M::ACC];
+    __shared__ int32_t sFirst[GPT];
+    __shared__ uint32_t sMask[GPT];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t item = blockIdx.x;
+    const int32_t split = item % nsplit, tt = item / nsplit;
+    const int32_t ct = tt / otiles, ot = tt - ct * otiles;
+    const int32_t c0 = ct * 32, o0 = ot * 32, g0 = o0 / N;
+
+    // ---- The tile's col-groups' kept blocks among channels [c0, c0 + 32).
+    if (tid < GPT) {
+        const int32_t g = g0 + tid;
+        uint32_t mask = 0;
+        int32_t first = 0;
+        if (g < a.G) {
+            const __amdgpu_buffer_rsrc_t rI = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<int32_t*>(a.I), 0, a.t * 4, kRawBufferFlags);
+            int32_t zb, ze;
+            group_range(a, g, zb, ze);
+            first = run_first(rI, zb, ze, c0);
+            for (int k = 0; k < 32; ++k) {
+                const int32_t e = first + k;
+                const int32_t c = e < ze ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rI, e * 4, 0, 0)) : INT32_MAX;
+                if (c < c0 + 32 && c < a.m) mask |= 1u << (c - c0);
+            }
+        }
+        sFirst[tid] = first;
+        sMask[tid] = mask;
+    }
+    __syncthreads();
+    uint32_t anyk = 0;
+#pragma unroll
+    for (int j = 0; j < GPT; ++j) anyk |= sMask[j];
+    if (anyk == 0) return;                     // (uniform) no kept block in the tile
+
+    const int32_t pb = int32_t(int64_t(a.npix) * split / nsplit) & ~(Q - 1);
+    const int32_t pe = split + 1 == nsplit ? a.npix : int32_t(int64_t(a.npix) * (split + 1) / nsplit) & ~(Q - 1);
+    const int pq = tid % QPR, rg = tid / QPR;
+    const int32_t HWo = a.HWo;
+    const int32_t batch = a.npix / HWo;
+    const uint32_t chb = uint32_t(HWo) * 4;    // channel stride of both X and dY (stride 1, no padding)
+    const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HWo * 4)),
+        kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
+        kRawBufferFlags);
+    uint32_t xr[RPT], yr[RPT];                 // row offsets (bytes), or out of range
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+        const int32_t r = rg + RG * j;
+        xr[j] = c0 + r < a.m ? uint32_t(c0 + r) * chb : kBufferOutOfRange;
+        yr[j] = o0 + r < a.n ? uint32_t(o0 + r) * chb : kBufferOutOfRange;
+    }
+    vq_t vx[RPT], vy[RPT];
+    auto load = [&](int32_t p0) __attribute__((always_inline)) {
+        const int32_t p = p0 + Q * pq;
+        const bool in = p < pe;
+        const int32_t b = in ? p / HWo : 0, hw = p - b * HWo;
+        const uint32_t bx = uint32_t((int64_t(b) * a.m * HWo + hw) * 4);
+        const uint32_t by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const bool okx = in && xr[j] != kBufferOutOfRange, oky = in && yr[j] != kBufferOutOfRange;
+            const int32_t ox = int32_t(okx ? bx + xr[j] : kBufferOutOfRange);
+            const int32_t oy = int32_t(oky ? by + yr[j] : kBufferOutOfRange);
+            if constexpr (Q == 4) {
+                vx[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rX, ox, 0, 0));
+                vy[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rY, oy, 0, 0));
+            } else {
+                vx[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rX, ox, 0, 0));
+                vy[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rY, oy, 0, 0));
+            }
+        }
+    };
+    auto put = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            *reinterpret_cast<vq_t*>(&sX[(rg + RG * j) * P + Q * pq]) = vx[j];
+            *reinterpret_cast<vq_t*>(&sY[(rg + RG * j) * P + Q * pq]) = vy[j];
+        }
+    };
+
+    acc_t acc;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) acc[r] = 0.f;
+    // Lane (row rc, group k): step s takes pixel k * 16 + s of the wave's 32.
+    const int rc = lane & 31, k = lane >> 5;
+    const float* ax = sX + rc * P + wave * 32 + k * PPL;
+    const float* ay = sY + rc * P + wave * 32 + k * PPL;
+    if (pb < pe) {
+        load(pb);
+        for (int32_t p0 = pb; p0 < pe; p0 += kBwCh) {
+            __syncthreads();   // the previous chunk's reads are done
+            put();
+            __syncthreads();
+            if (p0 + kBwCh < pe) load(p0 + kBwCh);
+#pragma unroll
+            for (int v = 0; v < PPL / 4; ++v) {
+                const f32x4 av = *reinterpret_cast<const f32x4*>(ax + 4 * v);
+                const f32x4 bv = *reinterpret_cast<const f32x4*>(ay + 4 * v);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = M::step(av[e], bv[e], acc);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) sR[wave][r * 64 + lane] = acc[r];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r)
+        acc[r] = ((sR[0][r * 64 + lane] + sR[1][r * 64 + lane]) + sR[2][r * 64 + lane]) + sR[3][r * 64 + lane];
+    // MFMA (row, col) = (input channel c0 + row, output channel o0 + col):
+    // stored where col-group (o0 + col) / N keeps the channel.
+    const int32_t oc = rc;                     // column within the tile
+    const int gs = oc / N, i = oc % N;         // col-group slot and block row
+    const uint32_t mask = sMask[gs];
+    const int32_t first = sFirst[gs];
+#pragma unroll
+    for (int r = 0; r < M::ACC; ++r) {
+        const int row = M::row(lane, r);
+        if (!((mask >> row) & 1)) continue;
+        const int32_t z = first + __builtin_popcount(mask & ((1u << row) - 1));
+        float* dst = dD + int64_t(z) * N + i;
+        if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
+        else *dst = acc[r];
+    }
+}
+
 }  // namespace
+
+// 1x1 stride-1 unpadded layers at N = 2, 4, 8: the dense-product kernel.
+static bool dense_dd(const ConvArgs& a) {
+    return (a.N == 2 || a.N == 4 || a.N == 8) && a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0;
+}
 
 bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
     if (xdt != ONEXN_F32) return false;
-    if (a.N != 16 && a.N != 32) return false;
+    if (a.N != 16 && a.N != 32 && !dense_dd(a)) return false;
     if (a.KK > 63) return false;   // one bit per tap, 63 meaning "no pair"
     if (int64_t(batch) * a.n * a.HWo * 4 >= (int64_t(1) << 31) ||
         int64_t(batch) * a.m * a.H * a.W * 4 >= (int64_t(1) << 31))
@@ -1073,7 +1249,40 @@ bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
     return true;
 }
 
+static onexn_status launch_bwd_weight_dense(const ConvArgs& a, const void* x, const void* dy, float* dD,
+                                           hipStream_t s) {
+    const int64_t ctiles = (int64_t(a.m) + 31) / 32, otiles = (int64_t(a.n) + 31) / 32;
+    const int64_t tiles = ctiles * otiles;
+    int64_t nsplit = (4 * int64_t(device_cu_count()) + tiles - 1) / tiles;
+    nsplit = std::max<int64_t>(1, std::min<int64_t>(nsplit, a.npix / 1024));
+    if (tuning(kTuneBwdSplit) >= 1) nsplit = tuning(kTuneBwdSplit);
+    const int64_t grid = tiles * nsplit;
+    if (grid < 1 || grid > INT32_MAX) return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_weight: grid out of range");
+    if (nsplit > 1) {
+        const int64_t n = int64_t(a.t) * a.N;
+        hipLaunchKernelGGL(bw_zero, dim3(uint32_t(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256), 0, s, dD, n);
+        const hipError_t zerr = hipGetLastError();
+        if (zerr != hipSuccess)
+            return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(zerr));
+    }
+    const bool quads = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(dy) & 15) == 0;
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a, static_cast<const float*>(x),
+                           static_cast<const float*>(dy), dD, int32_t(otiles), int32_t(nsplit));
+    };
+    switch (a.N) {
+        case 8: quads ? go(bwd_weight_dense<8, 4>) : go(bwd_weight_dense<8, 1>); break;
+        case 4: quads ? go(bwd_weight_dense<4, 4>) : go(bwd_weight_dense<4, 1>); break;
+        default: quads ? go(bwd_weight_dense<2, 4>) : go(bwd_weight_dense<2, 1>); break;
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(err));
+    return ONEXN_OK;
+}
+
 onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* dy, float* dD, hipStream_t s) {
+    if (dense_dd(a)) return launch_bwd_weight_dense(a, x, dy, dD, s);
     // A col-group keeps at most m blocks: m * KK pairs.
     const int64_t tiles_per_g = (int64_t(a.m) * a.KK + a.N - 1) / a.N;
     const int64_t tiles = (int64_t(a.t) * a.KK + a.N - 1) / a.N + a.G;   // tiles with pairs, at most

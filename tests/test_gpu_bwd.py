@@ -208,6 +208,33 @@ def test_bwd_kxk_kernels_agree_with_oracle(kernel, geom, N, tune):
     np.testing.assert_array_equal(dD, ref_dD)
 
 
+@pytest.mark.parametrize("split", ["default", "3"])
+@pytest.mark.parametrize("hw", [(8, 8), (7, 5)], ids=["quads", "no_quads"])
+@pytest.mark.parametrize("N", [2, 4, 8])
+def test_bwd_1x1_small_n(N, hw, split, tune):
+    """1x1 layers at N = 2 / 4 / 8 on the matrix cores: the input gradient with
+    256/N col-groups per stage, the weight gradient as the dense product of
+    32-channel tiles stored at the kept blocks (staged in pixel quads where
+    the images allow, one pixel per access otherwise; one pixel range per
+    tile and three added with atomics).  fp32 random 70 -> 100 (three channel
+    tiles, ragged col-group tiles) within 1e-5, and integer data exactly."""
+    if split != "default":
+        tune("bwd_split", int(split))
+    H, W = hw
+    gen = torch.Generator().manual_seed(41 + N + H)
+    w = workloads.gen_weight(gen, 100, 70, 1)
+    x = workloads.gen_activation(gen, (2, 70, H, W))
+    dy = torch.randn((2, 100, H, W), generator=gen)
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, 0.5, 1, 0)
+    assert rel_err(dx, ref_dx) <= 1e-5
+    assert rel_err(dD, ref_dD) <= 1e-5
+    wi, xi = workloads.gen_integer_layer(seed=N + W, cout=66, cin=40, k=1, batch=3, H=H, W=W, wmax=2, xmax=2)
+    dyi = torch.randint(-2, 3, (3, 66, H, W), generator=gen).float()
+    dx, dD, ref_dx, ref_dD = _bwd(wi, xi, dyi, N, 0.5, 1, 0)
+    np.testing.assert_array_equal(dx, ref_dx)
+    np.testing.assert_array_equal(dD, ref_dD)
+
+
 @pytest.mark.parametrize("k,N", [(3, 16), (1, 32)])
 def test_bwd_everything_pruned(k, N):
     w, x = workloads.gen_integer_layer(seed=1, cout=32, cin=5, k=k, batch=1, H=6)
