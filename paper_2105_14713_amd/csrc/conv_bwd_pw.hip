@@ -1,5 +1,5 @@
 // Input gradient of 1x1 (any stride, no padding; N in {2, 4, 8, 16, 32}) and
-// 3x3 (stride 1 or 2; N in {16, 32}) 1xN-pruned convolutions on matrix
+// 3x3 (stride 1 or 2; N in {8, 16, 32}) 1xN-pruned convolutions on matrix
 // cores: fp32, NCHW.
 //
 // Paper: Lin et al., "1xN Pattern for Pruning Convolutional Neural Networks"
@@ -678,7 +678,7 @@ bool bwd_data_pw_applies(const ConvArgs& a, onexn_dtype wdt, onexn_dtype dxdt, i
     const bool pw = a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0 &&                     // any stride,
                     (a.N == 2 || a.N == 4 || a.N == 8 || a.N == 16 || a.N == 32);        // N >= 2
     const bool k3 = a.kh == 3 && a.kw == 3 && a.sh == a.sw && (a.sh == 1 || a.sh == 2) &&   // any padding
-                    (a.N == 16 || a.N == 32);
+                    (a.N == 8 || a.N == 16 || a.N == 32);
     if (!pw && !k3) return false;
     if (int64_t(a.t) * a.N * a.KK * 4 >= (int64_t(1) << 31)) return false;   // D through a buffer
     if (a.G > kBpMaxG) return false;
@@ -705,16 +705,14 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
             case 4: hipLaunchKernelGGL(bwd_data_pw<4>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
             default: hipLaunchKernelGGL(bwd_data_pw<2>, grid, dim3(kBpThreads), 0, s, a, y, x); break;
         }
-    } else if (a.sh == 1) {
-        if (a.N == 32)
-            hipLaunchKernelGGL((bwd_data_k3<32, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
-        else
-            hipLaunchKernelGGL((bwd_data_k3<16, 1>), grid, dim3(kBpThreads), 0, s, a, y, x);
-    } else if (tuning(kTuneBwdKernel) == 2) {   // all nine taps for every pixel
-        if (a.N == 32)
-            hipLaunchKernelGGL((bwd_data_k3<32, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
-        else
-            hipLaunchKernelGGL((bwd_data_k3<16, 2>), grid, dim3(kBpThreads), 0, s, a, y, x);
+    } else if (a.sh == 1 || tuning(kTuneBwdKernel) == 2) {   // stride 2 here: all nine taps per pixel
+        auto go = [&](auto k32, auto k16, auto k8) {
+            if (a.N == 32) hipLaunchKernelGGL(k32, grid, dim3(kBpThreads), 0, s, a, y, x);
+            else if (a.N == 16) hipLaunchKernelGGL(k16, grid, dim3(kBpThreads), 0, s, a, y, x);
+            else hipLaunchKernelGGL(k8, grid, dim3(kBpThreads), 0, s, a, y, x);
+        };
+        if (a.sh == 1) go(bwd_data_k3<32, 1>, bwd_data_k3<16, 1>, bwd_data_k3<8, 1>);
+        else go(bwd_data_k3<32, 2>, bwd_data_k3<16, 2>, bwd_data_k3<8, 2>);
     } else {
         // One launch per parity class: pixels (2i + ca, 2j + cb) take the taps
         // of parities ((ca + ph) % 2, (cb + pw) % 2).
@@ -724,17 +722,16 @@ onexn_status launch_bwd_data_pw(const ConvArgs& a, const void* dy, void* dx, hip
                 const int64_t cpix = int64_t(batch) * ((a.H - ca + 1) / 2) * ((a.W - cb + 1) / 2);
                 const dim3 cgrid{uint32_t((cpix + kBpPix - 1) / kBpPix * ctiles), 1, 1};
                 const int cls = ((ca + a.ph) & 1) << 1 | ((cb + a.pw) & 1);
-                auto go = [&](auto k32, auto k16) {
-                    if (a.N == 32)
-                        hipLaunchKernelGGL(k32, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
-                    else
-                        hipLaunchKernelGGL(k16, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
+                auto go = [&](auto k32, auto k16, auto k8) {
+                    if (a.N == 32) hipLaunchKernelGGL(k32, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
+                    else if (a.N == 16) hipLaunchKernelGGL(k16, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
+                    else hipLaunchKernelGGL(k8, cgrid, dim3(kBpThreads), 0, s, a, y, x, ca, cb);
                 };
                 switch (cls) {
-                    case 0: go(bwd_data_s2<32, 0, 0>, bwd_data_s2<16, 0, 0>); break;
-                    case 1: go(bwd_data_s2<32, 0, 1>, bwd_data_s2<16, 0, 1>); break;
-                    case 2: go(bwd_data_s2<32, 1, 0>, bwd_data_s2<16, 1, 0>); break;
-                    default: go(bwd_data_s2<32, 1, 1>, bwd_data_s2<16, 1, 1>); break;
+                    case 0: go(bwd_data_s2<32, 0, 0>, bwd_data_s2<16, 0, 0>, bwd_data_s2<8, 0, 0>); break;
+                    case 1: go(bwd_data_s2<32, 0, 1>, bwd_data_s2<16, 0, 1>, bwd_data_s2<8, 0, 1>); break;
+                    case 2: go(bwd_data_s2<32, 1, 0>, bwd_data_s2<16, 1, 0>, bwd_data_s2<8, 1, 0>); break;
+                    default: go(bwd_data_s2<32, 1, 1>, bwd_data_s2<16, 1, 1>, bwd_data_s2<8, 1, 1>); break;
                 }
                 const hipError_t cerr = hipGetLastError();
                 if (cerr != hipSuccess)

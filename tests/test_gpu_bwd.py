@@ -64,6 +64,9 @@ CASES = [  # (n, m, k, stride, pad, B, H, W, N)
     (36, 33, 3, 2, 2, 1, 11, 12, 16),   # ragged last col-group
     (300, 40, 3, 2, 1, 1, 9, 9, 32),    # ten col-groups, the last ragged
     (32, 20, 3, 1, 2, 3, 5, 4, 16),     # padding wider than the map's margin
+    # 3x3 at N = 8: the matrix-core input gradient (stride 1, and stride 2 by parity class)
+    (48, 40, 3, 1, 1, 2, 9, 10, 8),
+    (36, 33, 3, 2, 1, 1, 11, 12, 8),
     # at most four input channels: the one-lane-per-pixel input gradient
     (20, 4, 3, 1, 1, 2, 9, 7, 4),
     (33, 1, 5, 3, 2, 1, 11, 13, 8),     # stride 3, output channels not a multiple of 8
@@ -177,7 +180,7 @@ def test_bwd_1x1_kernels_agree_with_oracle(kernel, N, tune):
 
 @pytest.mark.parametrize("kernel", ["matrix", "matrix_split3", "general", "nine_taps"])
 @pytest.mark.parametrize("geom", [(3, 1, 1), (3, 2, 1), (3, 2, 0), (7, 2, 3)], ids=["3x3s1", "3x3s2", "3x3s2p0", "7x7s2"])
-@pytest.mark.parametrize("N", [16, 32])
+@pytest.mark.parametrize("N", [8, 16, 32])
 def test_bwd_kxk_kernels_agree_with_oracle(kernel, geom, N, tune):
     """The k x k gradients through the matrix-core kernels (weight gradient
     over (block, tap) pair tiles with one pixel range per tile and with three;
