@@ -227,8 +227,8 @@ onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, 
  * Both accumulate in fp32.  The input gradient, and the weight gradient of
  * every layer except those below, sum in a fixed order (results do not vary
  * run to run).  For fp32 layers at N = 16 or 32 with few tiles of (kept
- * block, tap) pairs, and fp32 1x1 stride-1 unpadded layers at N = 2, 4, 8
- * with few 32 x 32 channel tiles (fewer than four workgroups per CU), the
+ * block, tap) pairs, and fp32 layers at N = 2, 4, 8 with few (32 x 32
+ * channel tile, tap) items (fewer than four workgroups per CU), the
  * weight gradient
  * splits the pixels over workgroups and adds their sums with atomics into the
  * zeroed dD, so the last bits can vary run to run; setting the tuning

@@ -1065,18 +1065,19 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_q4(ConvArgs a, const fl
 }
 
 
-// Weight gradient of 1x1 stride-1 unpadded layers at N <= 8, where an N x N
-// tile would leave the matrix cores mostly idle: the dense product
-//     G[c][o] = sum over pixels of X[c][pixel] * dY[o][pixel]
+// Weight gradient at N <= 8, where an N x N tile would leave the matrix
+// cores mostly idle: for each tap (q, r) the dense product
+//     G[c][o] = sum over output pixels of X[c][oh*sh - ph + q][ow*sw - pw + r] * dY[o][oh][ow]
 // of a tile of 32 input channels and 32 output channels (32/N col-groups)
 // on v_mfma_f32_32x32x2f32, of which only the entries of kept blocks are
-// stored: dD[z][i] = G[I[z]][gN + i] (at p = 0.5 half the tile's work is for
-// pruned blocks).  Items are (channel tile, output-channel tile, pixel
-// range); a prologue finds each of the tile's col-groups' kept blocks among
+// stored: dD[z][i][q][r] = G[I[z]][gN + i] (at p = 0.5 half the tile's work
+// is for pruned blocks).  Items are (channel tile, tap, output-channel tile,
+// pixel range); a prologue finds each of the tile's col-groups' kept blocks among
 // the 32 channels (first block and channel mask, as in the input
 // gradient), and a tile that holds none returns.  Chunks of 128 pixels are
-// staged as in bwd_weight_q4 (Q = 4: 16-byte pixel quads, images of a
-// multiple of 4 pixels) or one pixel per access (Q = 1); four waves split a
+// staged as in bwd_weight_q4 (Q = 4: 16-byte pixel quads, 1x1 stride-1
+// unpadded layers with images of a multiple of 4 pixels) or one pixel per
+// access (Q = 1, any kernel, stride and padding); four waves split a
 // chunk's pixels and add their sums in wave order.  Each dD entry belongs to
 // one tile: stored once, or added with atomics when pixel ranges split.
 template <int N, int Q>
@@ -1104,7 +1105,9 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int32_t item = blockIdx.x;
     const int32_t split = item % nsplit, tt = item / nsplit;
-    const int32_t ct = tt / otiles, ot = tt - ct * otiles;
+    const int32_t ot = tt % otiles, ctap = tt / otiles;
+    const int32_t tap = ctap % a.KK, ct = ctap / a.KK;
+    const int32_t tq = tap / a.kw, tr = tap - tq * a.kw;   // the tile's tap (q, r)
     const int32_t c0 = ct * 32, o0 = ot * 32, g0 = o0 / N;
 
     // ---- The tile's col-groups' kept blocks among channels [c0, c0 + 32).
@@ -1136,11 +1139,11 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const
     const int32_t pb = int32_t(int64_t(a.npix) * split / nsplit) & ~(Q - 1);
     const int32_t pe = split + 1 == nsplit ? a.npix : int32_t(int64_t(a.npix) * (split + 1) / nsplit) & ~(Q - 1);
     const int pq = tid % QPR, rg = tid / QPR;
-    const int32_t HWo = a.HWo;
+    const int32_t HWo = a.HWo, HW = a.H * a.W;
     const int32_t batch = a.npix / HWo;
-    const uint32_t chb = uint32_t(HWo) * 4;    // channel stride of both X and dY (stride 1, no padding)
+    const uint32_t chb = uint32_t(HWo) * 4, xchb = uint32_t(HW) * 4;   // channel strides of dY and X
     const __amdgpu_buffer_rsrc_t rX = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HWo * 4)),
+        const_cast<float*>(x), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.m * HW * 4)),
         kRawBufferFlags);
     const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(dy), 0, __builtin_amdgcn_readfirstlane(int32_t(int64_t(batch) * a.n * HWo * 4)),
@@ -1149,19 +1152,25 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
         const int32_t r = rg + RG * j;
-        xr[j] = c0 + r < a.m ? uint32_t(c0 + r) * chb : kBufferOutOfRange;
+        xr[j] = c0 + r < a.m ? uint32_t(c0 + r) * xchb : kBufferOutOfRange;
         yr[j] = o0 + r < a.n ? uint32_t(o0 + r) * chb : kBufferOutOfRange;
     }
     vq_t vx[RPT], vy[RPT];
     auto load = [&](int32_t p0) __attribute__((always_inline)) {
         const int32_t p = p0 + Q * pq;
-        const bool in = p < pe;
-        const int32_t b = in ? p / HWo : 0, hw = p - b * HWo;
-        const uint32_t bx = uint32_t((int64_t(b) * a.m * HWo + hw) * 4);
+        const bool pin = p < pe;
+        const int32_t b = pin ? p / HWo : 0, hw = p - b * HWo;
+        // Output pixel p reads input pixel (oh*sh - ph + q, ow*sw - pw + r)
+        // under the tile's tap, zero outside the image (pixel quads: 1x1
+        // stride 1 unpadded only, where that is pixel hw itself).
+        const int32_t oh = hw / a.Wo, ow = hw - oh * a.Wo;
+        const int32_t ih = oh * a.sh - a.ph + tq, iw = ow * a.sw - a.pw + tr;
+        const bool in = pin && uint32_t(ih) < uint32_t(a.H) && uint32_t(iw) < uint32_t(a.W);
+        const uint32_t bx = uint32_t((int64_t(b) * a.m * HW + int64_t(ih) * a.W + iw) * 4);
         const uint32_t by = uint32_t((int64_t(b) * a.n * HWo + hw) * 4);
 #pragma unroll
         for (int j = 0; j < RPT; ++j) {
-            const bool okx = in && xr[j] != kBufferOutOfRange, oky = in && yr[j] != kBufferOutOfRange;
+            const bool okx = in && xr[j] != kBufferOutOfRange, oky = pin && yr[j] != kBufferOutOfRange;
             const int32_t ox = int32_t(okx ? bx + xr[j] : kBufferOutOfRange);
             const int32_t oy = int32_t(oky ? by + yr[j] : kBufferOutOfRange);
             if constexpr (Q == 4) {
@@ -1223,7 +1232,7 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const
         const int row = M::row(lane, r);
         if (!((mask >> row) & 1)) continue;
         const int32_t z = first + __builtin_popcount(mask & ((1u << row) - 1));
-        float* dst = dD + int64_t(z) * N + i;
+        float* dst = dD + (int64_t(z) * N + i) * a.KK + tap;
         if (nsplit > 1) unsafeAtomicAdd(dst, acc[r]);
         else *dst = acc[r];
     }
@@ -1231,10 +1240,8 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_dense(ConvArgs a, const
 
 }  // namespace
 
-// 1x1 stride-1 unpadded layers at N = 2, 4, 8: the dense-product kernel.
-static bool dense_dd(const ConvArgs& a) {
-    return (a.N == 2 || a.N == 4 || a.N == 8) && a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0;
-}
+// Layers at N = 2, 4, 8: the dense-product kernel.
+static bool dense_dd(const ConvArgs& a) { return a.N == 2 || a.N == 4 || a.N == 8; }
 
 bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
     if (xdt != ONEXN_F32) return false;
@@ -1249,20 +1256,21 @@ bool bwd_weight_pw_applies(const ConvArgs& a, onexn_dtype xdt, int32_t batch) {
 static onexn_status launch_bwd_weight_dense(const ConvArgs& a, const void* x, const void* dy, float* dD,
                                            hipStream_t s) {
     const int64_t ctiles = (int64_t(a.m) + 31) / 32, otiles = (int64_t(a.n) + 31) / 32;
-    const int64_t tiles = ctiles * otiles;
+    const int64_t tiles = ctiles * a.KK * otiles;
     int64_t nsplit = (4 * int64_t(device_cu_count()) + tiles - 1) / tiles;
     nsplit = std::max<int64_t>(1, std::min<int64_t>(nsplit, a.npix / 1024));
     if (tuning(kTuneBwdSplit) >= 1) nsplit = tuning(kTuneBwdSplit);
     const int64_t grid = tiles * nsplit;
     if (grid < 1 || grid > INT32_MAX) return fail(ONEXN_ERR_UNSUPPORTED, "conv2d_bwd_weight: grid out of range");
     if (nsplit > 1) {
-        const int64_t n = int64_t(a.t) * a.N;
+        const int64_t n = int64_t(a.t) * a.N * a.KK;
         hipLaunchKernelGGL(bw_zero, dim3(uint32_t(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256), 0, s, dD, n);
         const hipError_t zerr = hipGetLastError();
         if (zerr != hipSuccess)
             return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(zerr));
     }
-    const bool quads = a.HWo % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+    const bool quads = a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0 && a.HWo % 4 == 0 &&
+                       (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(dy) & 15) == 0;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a, static_cast<const float*>(x),
