@@ -1270,7 +1270,7 @@ static onexn_status launch_bwd_weight_dense(const ConvArgs& a, const void* x, co
             return fail(ONEXN_ERR_HIP, "conv2d_bwd_weight: launch failed: %s", hipGetErrorString(zerr));
     }
     const bool quads = a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0 && a.HWo % 4 == 0 &&
-                       (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                       tuning(kTuneBwdKernel) != 3 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(dy) & 15) == 0;
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, dim3(uint32_t(grid)), dim3(kBwThreads), 0, s, a, static_cast<const float*>(x),
@@ -1313,7 +1313,7 @@ onexn_status launch_bwd_weight_pw(const ConvArgs& a, const void* x, const void* 
     };
     // 1x1 stride-1 unpadded layers with whole pixel quads per image: quads.
     const bool quads = a.KK == 1 && a.sh == 1 && a.sw == 1 && a.ph == 0 && a.pw == 0 && a.HWo % 4 == 0 &&
-                       (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                       tuning(kTuneBwdKernel) != 3 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
                        tuning(kTuneBwdKernel) != 3;
     if (a.N == 32) {
         if (quads) go(bwd_weight_q4<32>);
