@@ -238,6 +238,45 @@ def test_bwd_1x1_small_n(N, hw, split, tune):
     np.testing.assert_array_equal(dD, ref_dD)
 
 
+def _fuzz_cases(count, seed):
+    """Seeded random small layers spanning the backward dispatch: N, kernel
+    size, stride, padding, channel counts (ragged col-groups and channel
+    tiles), map sizes (pixel quads or not), batch and p."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        N = int(rng.choice([1, 2, 4, 8, 16, 32]))
+        k = int(rng.choice([1, 1, 3, 3, 5, 7]))
+        s = int(rng.choice([1, 1, 2, 3]))
+        pd = int(rng.integers(0, (k + 1) // 2 + 1))
+        H, W = int(rng.integers(k, 15)), int(rng.integers(k, 15))
+        if (H + 2 * pd - k) // s + 1 < 1 or (W + 2 * pd - k) // s + 1 < 1:
+            continue
+        n = int(rng.integers(1, 3 * N + 40))
+        m = int(rng.integers(1, 90))
+        B = int(rng.integers(1, 4))
+        p = float(rng.choice([0.0, 0.5, 0.9]))
+        cases.append((n, m, k, s, pd, B, H, W, N, p))
+    return cases
+
+
+@pytest.mark.parametrize("case", _fuzz_cases(80, 2024),
+                         ids=lambda c: "n%d_m%d_k%d_s%d_p%d_B%d_%dx%d_N%d_p%g" % c)
+def test_bwd_fuzz_integer_exact(case):
+    """Both gradients integer-exact against the oracle on 80 seeded random
+    small layers (outputs pre-filled with NaN)."""
+    n, m, k, s, pd, B, H, W, N, p = case
+    print(f"bwd fuzz {case}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=n * 7 + m + k, cout=n, cin=m, k=k, batch=B, H=H, W=W,
+                                       wmax=2, xmax=2)
+    Ho, Wo = (H + 2 * pd - k) // s + 1, (W + 2 * pd - k) // s + 1
+    gen = torch.Generator().manual_seed(n + 13 * m)
+    dy = torch.randint(-2, 3, (B, n, Ho, Wo), generator=gen).float()
+    dx, dD, ref_dx, ref_dD = _bwd(w, x, dy, N, p, s, pd)
+    np.testing.assert_array_equal(dx, ref_dx)
+    np.testing.assert_array_equal(dD, ref_dD)
+
+
 @pytest.mark.parametrize("k,N", [(3, 16), (1, 32)])
 def test_bwd_everything_pruned(k, N):
     w, x = workloads.gen_integer_layer(seed=1, cout=32, cin=5, k=k, batch=1, H=6)
