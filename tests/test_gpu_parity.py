@@ -631,3 +631,45 @@ def test_pw_direct_integer_exact(case, tile, kdb, tune):
         y, _ = gpu_conv(w, x, c["N"], p, True, c["s"], c["pd"])
         ref, _ = oracle_conv(w, x, c["N"], p, True, c["s"], c["pd"])
         np.testing.assert_array_equal(y, ref)
+
+
+def _fwd_fuzz_cases(count, seed):
+    """Seeded random small layers spanning the forward dispatch: N, kernel
+    size, stride, padding, NCHW / NHWC, fp32 / bf16 inputs, channel counts
+    (ragged col-groups), map sizes, batch, p and the rearrangement."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        N = int(rng.choice([1, 2, 4, 8, 16, 32]))
+        k = int(rng.choice([1, 1, 1, 3, 3, 5, 7]))
+        s = int(rng.choice([1, 1, 2, 3]))
+        pd = int(rng.integers(0, (k + 1) // 2 + 1))
+        H, W = int(rng.integers(k, 17)), int(rng.integers(k, 17))
+        if (H + 2 * pd - k) // s + 1 < 1 or (W + 2 * pd - k) // s + 1 < 1:
+            continue
+        n = int(rng.integers(1, 3 * N + 40))
+        m = int(rng.integers(1, 120))
+        B = int(rng.integers(1, 4))
+        p = float(rng.choice([0.0, 0.5, 0.9]))
+        layout = str(rng.choice(["nchw", "nchw", "nhwc"]))
+        dt = str(rng.choice(["f32", "f32", "bf16"]))
+        re = bool(rng.integers(0, 2))
+        cases.append((n, m, k, s, pd, B, H, W, N, p, layout, dt, re))
+    return cases
+
+
+@pytest.mark.parametrize("case", _fwd_fuzz_cases(120, 7),
+                         ids=lambda c: "n%d_m%d_k%d_s%d_p%d_B%d_%dx%d_N%d_p%g_%s_%s_re%d" % c)
+def test_conv_fuzz_integer_exact(case):
+    """The forward integer-exact against the oracle on 120 seeded random small
+    layers (outputs pre-filled with NaN; bf16 inputs write fp32 outputs, so
+    the integer sums stay exact)."""
+    n, m, k, s, pd, B, H, W, N, p, layout, dt, re = case
+    print(f"conv fuzz {case}", flush=True)
+    w, x = workloads.gen_integer_layer(seed=n * 3 + m + k, cout=n, cin=m, k=k, batch=B, H=H, W=W,
+                                       wmax=2, xmax=2)
+    if dt == "bf16":
+        w, x = w.bfloat16(), x.bfloat16()
+    y, _ = gpu_conv(w, x, N, p, re, s, pd, layout, out_dtype=torch.float32)
+    ref, _ = oracle_conv(w.float(), x.float(), N, p, re, s, pd)
+    np.testing.assert_array_equal(y, ref)
