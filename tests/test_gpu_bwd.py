@@ -260,10 +260,10 @@ def _fuzz_cases(count, seed):
     return cases
 
 
-@pytest.mark.parametrize("case", _fuzz_cases(80, 2024),
+@pytest.mark.parametrize("case", _fuzz_cases(200, 2024),
                          ids=lambda c: "n%d_m%d_k%d_s%d_p%d_B%d_%dx%d_N%d_p%g" % c)
 def test_bwd_fuzz_integer_exact(case):
-    """Both gradients integer-exact against the oracle on 80 seeded random
+    """Both gradients integer-exact against the oracle on 200 seeded random
     small layers (outputs pre-filled with NaN)."""
     n, m, k, s, pd, B, H, W, N, p = case
     print(f"bwd fuzz {case}", flush=True)
