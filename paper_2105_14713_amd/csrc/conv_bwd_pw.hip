@@ -953,7 +953,6 @@ __global__ void __launch_bounds__(kBwThreads) bwd_weight_q4(ConvArgs a, const fl
                                                              int32_t nsplit) {
     typedef PwMfma<N> M;
     typedef typename M::acc_t acc_t;
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     constexpr int KS = M::KS;                  // lane groups = pixels per MFMA step
     constexpr int P = kBqPitch;
     constexpr int QPR = kBwCh / 4;             // pixel quads per chunk row
