@@ -130,10 +130,21 @@ def copy_calibration(dev):
                       "bytes_written": COPY_BYTES, "launches": 5}), flush=True)
 
 
-def parity_gate(prepared, wl):
+def epilogue_params(layer, li):
+    """Seeded per-channel parameters of a folded batch norm for layer ``li``
+    (scale in [0.5, 1.5), bias ~ N(0, 0.25^2), channel order of the layer's
+    output), as host float32 tensors."""
+    g = torch.Generator().manual_seed(10_000 + li)
+    scale = 0.5 + torch.rand(layer.cout, generator=g)
+    bias = 0.25 * torch.randn(layer.cout, generator=g)
+    return scale, bias
+
+
+def parity_gate(prepared, wl, fused=False):
     """Each layer's output (from one launch of the same call the timed steps
-    make) against the oracle at sampled outputs.  Returns per-layer records;
-    exits with status 3 on the first layer over the bar."""
+    make) against the oracle at sampled outputs (with the oracle's epilogue
+    when the layers carry a folded batch norm and ReLU).  Returns per-layer
+    records; exits with status 3 on the first layer over the bar."""
     import oracle
     bar = 2e-2 if wl.out_dtype == "bf16" else 1e-5
     recs = []
@@ -151,6 +162,12 @@ def parity_gate(prepared, wl):
         pr = oracle.prune(w_cpu.double().numpy(), layer.N, layer.p, layer.rearrange)
         ref = oracle.conv2d_at(x_cpu.double().numpy(), pr.wbar, idx, (layer.stride,) * 2,
                                (layer.pad,) * 2)
+        if fused:
+            # Each sample as a channel of its own: act(scale[o] * v + bias[o]).
+            o = (idx // (layer.Ho * layer.Ho)) % layer.cout
+            sc, bi = epilogue_params(layer, li)
+            ref = oracle.epilogue(ref.reshape(1, -1, 1), sc.double().numpy()[o],
+                                  bi.double().numpy()[o], "relu").reshape(-1)
         den = float(abs(ref).max()) if ref.size else 0.0
         num = float(abs(got - ref).max()) if ref.size else 0.0
         err = num / den if den > 0 else (0.0 if num == 0 else float("inf"))
@@ -354,6 +371,9 @@ def main():
                     help="time the backward kernels on the workload's layers instead of the forward")
     ap.add_argument("--mask", action="store_true",
                     help="time the GPU mask building of the workload's layers instead of the conv")
+    ap.add_argument("--fused", action="store_true",
+                    help="every layer with a folded batch norm and ReLU in its store stage "
+                         "(the fused entry point)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a copy kernel of known size (for scaling byte counters)")
     ap.add_argument("--tune", action="append", default=[], metavar="NAME=VALUE",
@@ -393,12 +413,17 @@ def main():
     f_act = f_dense = b_alg = 0.0
     t_host = 0.0
     peak = PEAK_TFLOPS[wl.dtype]
-    for layer in wl.layers:
+    for li, layer in enumerate(wl.layers):
         w, x = workloads.gen_layer(layer, batch, wl.dtype)
         t0 = time.perf_counter()
         packed = onexn.prepare_layer(w, layer.N, layer.p, layer.rearrange, dev)
         t_host += time.perf_counter() - t0
         fa, fd, bb = layer_work(layer, packed, batch, wl.dtype, wl.out_dtype)
+        ep = {}
+        if args.fused:
+            sc, bi = epilogue_params(layer, li)
+            ep = {"scale": sc.to(dev), "bias": bi.to(dev), "act": "relu"}
+            bb += 2 * 4 * layer.cout
         f_act, f_dense, b_alg = f_act + fa, f_dense + fd, b_alg + bb
         t_c, t_m = fa / (peak * 1e12), bb / (PEAK_HBM_GBPS * 1e9)
         rows.append({"layer": layer.name, "k": layer.k, "stride": layer.stride, "cin": layer.cin,
@@ -424,17 +449,18 @@ def main():
         ys = [torch.empty(yshape, dtype=odt, device=dev) for _ in range(copies)]
         if wl.fc_layout:
             calls = [(lambda r=r: onexn.fc_fwd(packed.P, packed.I, packed.D, packed.n, xs[r],
-                                               wl.fc_layout, odt, ys[r], stream.cuda_stream))
+                                               wl.fc_layout, odt, ys[r], stream.cuda_stream, **ep))
                      for r in range(copies)]
         else:
             calls = [onexn.BoundConv(packed.P, packed.I, packed.D, packed.n, xs[r], ys[r],
-                                     layer.stride, layer.pad, wl.layout, stream.cuda_stream)
+                                     layer.stride, layer.pad, wl.layout, stream.cuda_stream, **ep)
                      for r in range(copies)]
         prepared.append((layer, packed, xs, ys, w, x, calls))
 
     # Parity before timing: the same bound calls the timed steps issue.
     print("bench: parity gate against the oracle", file=sys.stderr, flush=True)
-    gate = parity_gate([(l, pk, xs, ys, w, x, calls[0]) for l, pk, xs, ys, w, x, calls in prepared], wl)
+    gate = parity_gate([(l, pk, xs, ys, w, x, calls[0]) for l, pk, xs, ys, w, x, calls in prepared], wl,
+                       args.fused)
     calls = [item[6] for item in prepared]
     del prepared    # the host copies of the inputs are no longer needed
 
@@ -527,7 +553,7 @@ def main():
         pk, unit = peak, "TFLOP/s"
     else:
         pk, unit = PEAK_HBM_GBPS, "GB/s"
-    traffic = measured_traffic(args.workload)
+    traffic = None if args.fused else measured_traffic(args.workload)
 
     rec = {
         "metric": METRIC,
@@ -567,6 +593,8 @@ def main():
         "host_enqueued_ahead": host_ahead,
         "host_launch_us_per_step": round(host_step_s * 1e6, 1),
     }
+    if args.fused:
+        rec["config"]["epilogue"] = "folded batch norm (per-channel scale and bias) + ReLU, fused"
     if args.tune:
         rec["config"]["tuning"] = args.tune
     if not args.no_cpu:

@@ -79,15 +79,20 @@ template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) { re
 // the instantiation without it has no epilogue code at all (its parameter
 // loads would otherwise make the stores wait for every load in flight).  The
 // branches are uniform (kernel arguments).
+// The activation of the fused epilogue (after scale and bias).
+__device__ __forceinline__ float epilogue_act(const ConvArgs& a, float v) {
+    if (a.ep_act == ONEXN_ACT_RELU) v = fmaxf(v, 0.f);
+    else if (a.ep_act == ONEXN_ACT_RELU6) v = fminf(fmaxf(v, 0.f), 6.f);
+    return v;
+}
+
 template <bool kEp = true>
 __device__ __forceinline__ float epilogue(const ConvArgs& a, int32_t o, float v) {
     if constexpr (!kEp) return v;
     if (a.ep_scale && a.ep_bias) v = fmaf(v, a.ep_scale[o], a.ep_bias[o]);
     else if (a.ep_scale) v *= a.ep_scale[o];
     else if (a.ep_bias) v += a.ep_bias[o];
-    if (a.ep_act == ONEXN_ACT_RELU) v = fmaxf(v, 0.f);
-    else if (a.ep_act == ONEXN_ACT_RELU6) v = fminf(fmaxf(v, 0.f), 6.f);
-    return v;
+    return epilogue_act(a, v);
 }
 
 inline bool has_epilogue(const ConvArgs& a) {

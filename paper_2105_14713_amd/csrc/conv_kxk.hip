@@ -53,6 +53,10 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
     static_assert(CC % KS == 0 && DBUF % 64 == 0, "chunk shape");
     extern __shared__ __attribute__((aligned(16))) float smem[];
     __shared__ int32_t sC[SPLIT ? kKxSplitMaxG + 1 : 1];   // chunks of the col-groups before g
+    // Fused epilogue (unsplit kernel: one col-group per workgroup): scale and
+    // bias of its N channels, staged at the start, read run by run at the
+    // store.
+    __shared__ __attribute__((aligned(16))) float sEp[kEp ? 2 * N : 4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -275,15 +279,35 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
 
     // Store: MFMA (row, col) of column block nb -> output channel g*N + row.
     float* __restrict__ y = static_cast<float*>(a.y);
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-        if (ybase[nb] < 0) continue;
+    if constexpr (kEp && !SPLIT) {
+        // Runs of four rows, each fenced off from the next: computed all at
+        // once, the epilogue's parameters and results would raise the
+        // register count far above what the main loop needs.
+        EpRows<N, true> ep;
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
+            if (r % 4 == 0) {
+                __builtin_amdgcn_sched_barrier(0);
+                ep.load_staged_run(sEp, sEp + N, 0, lane, r / 4);
+            }
             const int32_t oc = g * N + M::row(lane, r);
-            if (oc >= a.n) continue;
-            if (SPLIT && split) unsafeAtomicAdd(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
-            else store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[nb][r]));
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                if (ybase[nb] >= 0 && oc < a.n)
+                    store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], ep.apply(a, r, acc[nb][r]));
+        }
+    } else {
+        static_assert(!kEp, "the split kernel adds raw sums: no epilogue");
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            if (ybase[nb] < 0) continue;
+#pragma unroll
+            for (int r = 0; r < M::ACC; ++r) {
+                const int32_t oc = g * N + M::row(lane, r);
+                if (oc >= a.n) continue;
+                if (SPLIT && split) unsafeAtomicAdd(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+                else store_out(&y[ybase[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            }
         }
     }
     };
@@ -293,6 +317,15 @@ __global__ void __launch_bounds__(kKxThreads) kxk_f32(ConvArgs a) {
         const int32_t g = L % a.G, tile = L / a.G;
         int32_t zb, ze;
         group_range(a, g, zb, ze);
+        if constexpr (kEp) {
+            // (visible at the store: the main loop has barriers)
+            const int tid = threadIdx.x;
+            if (tid < N) {
+                const int32_t o = g * N + tid;
+                sEp[tid] = o < a.n && a.ep_scale ? a.ep_scale[o] : 1.f;
+                sEp[N + tid] = o < a.n && a.ep_bias ? a.ep_bias[o] : 0.f;
+            }
+        }
         run(tile, g, 0, (ze - zb + CC - 1) / CC, false);
     } else {
         // Balanced split: the (tile, col-group, chunk) sequence, tile-major,

@@ -48,6 +48,9 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
     constexpr int UPW = 4 / KSPLIT;                 // units per workgroup
     constexpr int RED = KSPLIT > 1 ? 4 * NB * M::ACC * 64 : 1;
     __shared__ float sR[RED];
+    // Fused epilogue: scale and bias of each unit's N channels, staged when
+    // the unit starts and read back run by run at the store.
+    __shared__ __attribute__((aligned(16))) float sEp[kEp ? 4 * 2 * N : 4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -61,6 +64,13 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
     const bool live = pb < pblocks;
     int32_t zb = 0, ze = 0;
     if (live) group_range(a, g, zb, ze);
+    if constexpr (kEp) {
+        if (kq == 0 && lane < N) {
+            const int32_t o = g * N + lane;
+            sEp[uw * 2 * N + lane] = o < a.n && a.ep_scale ? a.ep_scale[o] : 1.f;
+            sEp[uw * 2 * N + N + lane] = o < a.n && a.ep_bias ? a.ep_bias[o] : 0.f;
+        }
+    }
     const int32_t per = (ze - zb + KSPLIT - 1) / KSPLIT;
     const int32_t z0 = min(ze, zb + kq * per), z1 = min(ze, z0 + per);
 
@@ -184,13 +194,33 @@ __global__ void __launch_bounds__(kDThreads) pw_direct(ConvArgs a) {
     if (!live) return;
 
     float* __restrict__ y = static_cast<float*>(a.y);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        if (yo[nb] < 0) continue;
+    if constexpr (kEp) {
+        // Runs of four rows, each fenced off from the next: computed all at
+        // once, the epilogue's parameters and results would raise the
+        // kernel's register count (and cut its occupancy) far above what its
+        // main loop needs.  (The wave wrote sEp itself; its LDS operations
+        // complete in order.)
+        EpRows<N, true> ep;
 #pragma unroll
         for (int r = 0; r < M::ACC; ++r) {
+            if (r % 4 == 0) {
+                __builtin_amdgcn_sched_barrier(0);
+                ep.load_staged_run(sEp + uw * 2 * N, sEp + uw * 2 * N + N, 0, lane, r / 4);
+            }
             const int32_t oc = g * N + M::row(lane, r);
-            if (oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[nb][r]));
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                if (yo[nb] >= 0 && oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], ep.apply(a, r, acc[nb][r]));
+        }
+    } else {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            if (yo[nb] < 0) continue;
+#pragma unroll
+            for (int r = 0; r < M::ACC; ++r) {
+                const int32_t oc = g * N + M::row(lane, r);
+                if (oc < a.n) store_out(&y[yo[nb] + int64_t(oc) * a.y_c], acc[nb][r]);
+            }
         }
     }
 }

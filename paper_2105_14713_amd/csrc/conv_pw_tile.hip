@@ -52,6 +52,7 @@ constexpr int kTileSteps = 4;                           // MFMA steps per block
 constexpr int kTileMaxG = 256;                          // col-groups a layer may have
 constexpr int32_t kBufferFlags = 0x00020000;            // buffer resource word 3: 32-bit raw data
 constexpr int kTileEarly = 32;                          // copies of the second tile issued before the first is awaited
+constexpr int kTileEpMax = 3072;                        // channels whose epilogue parameters LDS holds
 
 __device__ __forceinline__ int32_t lds_load(const int32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -75,6 +76,11 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     __shared__ __attribute__((aligned(16))) float sX[2 * kTileBufFloats + SW];
     __shared__ int32_t sP[kTileMaxG + 1];   // P[g] + g: cost of the units before group g
     __shared__ int32_t sNext[2], sReady[2], sLanded[2], sDone[2], sSetup;
+    // Fused epilogue: scale then bias of every channel of the col-groups
+    // (G * N <= kTileEpMax), staged once so that the stores inside the main
+    // loop read them from LDS: a global load there would make the store wait
+    // for every weight and index load the pipeline has in flight.
+    __shared__ __attribute__((aligned(16))) float sEp[kEp ? 2 * kTileEpMax : 4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -190,6 +196,13 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
         }
         for (int i = lane; i < SW; i += 64)
             if (wave == 0) sX[2 * kTileBufFloats + i] = 0.f;
+        if constexpr (kEp) {
+            for (int32_t i = tid; i < G * N; i += kTileCompute * 64) {
+                const bool in = i < a.n;
+                sEp[i] = in && a.ep_scale ? a.ep_scale[i] : 1.f;
+                sEp[kTileEpMax + i] = in && a.ep_bias ? a.ep_bias[i] : 0.f;
+            }
+        }
         wait_lgkm();
         if (lane == 0) atomicAdd(&sSetup, 1);
     }
@@ -333,8 +346,9 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
     // blocks): MFMA (row, col n) of block e -> output channel g*N + row,
     // pixel T*PT + slice*SW + NB*n + e.  Clears the accumulators.
     float* __restrict__ y = static_cast<float*>(a.y);
-    auto store_unit = [&](int32_t tile, int32_t slice, int32_t g, bool zeros) {
+    auto store_unit = [&](int32_t tile, int32_t slice, int32_t g, bool zeros) __attribute__((always_inline)) {
         const int32_t p0 = tile * PT + slice * SW + NB * lo;
+        EpRows<N, kEp> ep;
         if (kVec4) {
             // HWo % 4 == 0: an aligned run of NB <= 4 pixels lies in one image.
             if (p0 < a.npix) {
@@ -342,15 +356,17 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
                 float* yb = y + int64_t(b) * a.y_img + (p0 - b * a.HWo);
 #pragma unroll
                 for (int r = 0; r < M::ACC; ++r) {
+                    if (r % 4 == 0) ep.load_staged_run(sEp, sEp + kTileEpMax, g, lane, r / 4);
                     const int32_t o = g * N + M::row(lane, r);
                     if (o >= a.n) continue;
                     vec_t v;
 #pragma unroll
-                    for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, epilogue<kEp>(a, o, zeros ? 0.f : acc[e][r]));
+                    for (int e = 0; e < NB; ++e) vec_set<NB>(v, e, ep.apply(a, r, zeros ? 0.f : acc[e][r]));
                     store_out(reinterpret_cast<vec_t*>(yb + int64_t(o) * a.y_c), v);
                 }
             }
         } else {
+            ep.load_staged(sEp, sEp + kTileEpMax, g, lane);
 #pragma unroll
             for (int e = 0; e < NB; ++e) {
                 const int32_t p = p0 + e;
@@ -360,7 +376,7 @@ __global__ void __launch_bounds__(kTileThreads) pw_tile_f32(ConvArgs a) {
 #pragma unroll
                 for (int r = 0; r < M::ACC; ++r) {
                     const int32_t o = g * N + M::row(lane, r);
-                    if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], epilogue<kEp>(a, o, zeros ? 0.f : acc[e][r]));
+                    if (o < a.n) store_out(&y[yb + int64_t(o) * a.y_c], ep.apply(a, r, zeros ? 0.f : acc[e][r]));
                 }
             }
         }
@@ -548,6 +564,7 @@ onexn_status launch_tile_sw(ConvArgs a, hipStream_t s) {
 bool pw_tile_applies(const ConvArgs& a) {
     if (a.kh != 1 || a.kw != 1 || a.sh != 1 || a.sw != 1 || a.ph != 0 || a.pw != 0) return false;
     if (a.y_c != a.HWo || a.x_c != a.H * a.W) return false;   // NCHW
+    if (has_epilogue(a) && int64_t(a.G) * a.N > kTileEpMax) return false;   // parameters do not fit LDS
     return (a.N == 16 || a.N == 32) && tile_shape(a).sw > 0;
 }
 
