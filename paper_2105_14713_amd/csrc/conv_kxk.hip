@@ -452,6 +452,29 @@ __global__ void __launch_bounds__(256) kx_zero(float* __restrict__ p, int64_t n)
     }
 }
 
+// The fused epilogue over a finished NCHW output (n floats at p), for a
+// split launch: its parts add raw sums into y, so the epilogue can only
+// follow them.  Elements are numbered [image][channel][pixel]; n < 2^31.
+__global__ void __launch_bounds__(256) kx_epilogue(ConvArgs a, float* __restrict__ p, int32_t n) {
+    const int32_t stride = int32_t(gridDim.x) * 256 * 4;
+    for (int32_t i = (int32_t(blockIdx.x) * 256 + threadIdx.x) * 4; i < n; i += stride) {
+        if (i + 4 <= n) {
+            f32x4 v = *reinterpret_cast<const f32x4*>(p + i);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = epilogue(a, (i + j) / a.HWo % a.n, v[j]);
+            store_out(reinterpret_cast<f32x4*>(p + i), v);
+        } else {
+            for (int32_t j = i; j < n; ++j) p[j] = epilogue(a, j / a.HWo % a.n, p[j]);
+        }
+    }
+}
+
+// Largest output (bytes) for which a layer with an epilogue keeps the
+// balanced split and runs kx_epilogue after it, rather than taking the
+// unsplit kernel with the epilogue in its stores: the extra pass reads and
+// writes y once more, which the split's gain outweighs on small outputs only.
+constexpr int64_t kKxEpPassMax = int64_t(16) << 20;
+
 // Workgroups per compute unit of the balanced split (0: one workgroup per
 // output block).  All blocks of a launch are resident at once, so a launch
 // takes as long as its busiest compute unit: with few blocks per unit (800
@@ -482,13 +505,16 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
     a.kx_tiles = int32_t(tiles);
     const size_t lds = size_t(kx_lds_bytes(CC, s.cp, N, K * K));
     // (NCHW output, contiguous and 16-byte aligned for the zero fill.)
-    // (The parts of a split block add raw sums into y, so a fused epilogue
-    // takes the unsplit kernel.)
-    const bool can_split = !has_epilogue(a) && a.G <= kKxSplitMaxG && a.y_c == a.HWo &&
+    // (The parts of a split block add raw sums into y, so with a fused
+    // epilogue a small output takes the split and a pass of kx_epilogue, a
+    // larger one the unsplit kernel.)
+    const int64_t ny = int64_t(a.npix / a.HWo) * a.y_img;
+    const bool ep = has_epilogue(a);
+    const bool ep_ok = !ep || (ny * 4 <= kKxEpPassMax && a.y_img == int64_t(a.n) * a.HWo);
+    const bool can_split = ep_ok && a.G <= kKxSplitMaxG && a.y_c == a.HWo &&
                            reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
     const int split = can_split ? kx_split_choice(s, total) : 0;
     if (split > 0) {
-        const int64_t ny = int64_t(a.npix / a.HWo) * a.y_img;
         const int64_t zb = std::min<int64_t>((ny + 1023) / 1024, 4 * int64_t(device_cu_count()));
         hipLaunchKernelGGL(kx_zero, dim3(uint32_t(zb)), dim3(256), 0, stream, static_cast<float*>(a.y), ny);
         const hipError_t zerr = hipGetLastError();
@@ -497,6 +523,13 @@ onexn_status launch_nbw(ConvArgs a, const KxShape& s, hipStream_t stream) {
         // (Ranges shorter than an eighth of a block only add partial sums.)
         a.total = int32_t(std::min<int64_t>(8 * total, int64_t(split) * device_cu_count()));
         hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, true, false>), dim3(uint32_t(a.total)), dim3(kKxThreads), lds, stream, a);
+        if (ep) {
+            const hipError_t serr = hipGetLastError();
+            if (serr != hipSuccess)
+                return fail(ONEXN_ERR_HIP, "conv2d_fwd: launch failed: %s", hipGetErrorString(serr));
+            hipLaunchKernelGGL(kx_epilogue, dim3(uint32_t(zb)), dim3(256), 0, stream, a, static_cast<float*>(a.y),
+                               int32_t(ny));
+        }
     } else {
         if (has_epilogue(a))
             hipLaunchKernelGGL((kxk_f32<N, K, NBW, CC, false, true>), dim3(uint32_t(total)), dim3(kKxThreads), lds, stream, a);

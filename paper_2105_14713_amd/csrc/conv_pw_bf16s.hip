@@ -91,6 +91,9 @@ __device__ __forceinline__ int32_t ring_row_off(int32_t R) { return (R << 8) + (
 template <typename TY, bool kEp>
 __global__ void __launch_bounds__(kSThreads) pw_bf16s(ConvArgs a) {
     __shared__ __attribute__((aligned(16))) char sX[kSLds];
+    // Fused epilogue: one 64-entry slot per compute wave (its current
+    // col-group's 32 scales, then 32 biases).
+    __shared__ __attribute__((aligned(16))) float sEp[kEp ? kSCompute * 64 : 4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -273,6 +276,20 @@ __global__ void __launch_bounds__(kSThreads) pw_bf16s(ConvArgs a) {
         for (int u = 0; u < kSAhead - 1; ++u)
             if (j0 + u < it.nwin) process(u, j0 + u);
 
+        // Fused epilogue: the item's 32 scales (lanes 0-31) and biases (lanes
+        // 32-63) go to the wave's LDS slot here, where this item's loads have
+        // all been consumed, so the wait covers these loads alone; at the
+        // store (behind the next item's first loads) a global load would wait
+        // for those too.
+        if constexpr (kEp) {
+            if (it.g < a.G) {
+                const int32_t o = it.g * 32 + (lane & 31);
+                const bool in = o < a.n;
+                sEp[w * 64 + lane] = lane < 32 ? (in && a.ep_scale ? a.ep_scale[o] : 1.f)
+                                               : (in && a.ep_bias ? a.ep_bias[o] : 0.f);
+            }
+        }
+
         // The next item's first windows, then this item's stores.
         const Item nx = item_at(k + 1);
         if (k + 1 < nloc) {
@@ -290,14 +307,16 @@ __global__ void __launch_bounds__(kSThreads) pw_bf16s(ConvArgs a) {
                 const int32_t hw = 8 * (id - b * gpi) + (n & 7);
                 if (id >= ngran || hw >= a.HWo) continue;
                 TY* yb = y + int64_t(b) * a.y_img + hw;
+                EpRows<32, kEp> ep;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
+                    if (kEp && r % 4 == 0) ep.load_staged_run(sEp + w * 64, sEp + w * 64 + 32, 0, lane, r / 4);
                     const int32_t o = it.g * 32 + PwMfma<32>::row(lane, r);
                     // Plain stores: with 2-byte elements a half-wave writes
                     // 64 bytes of a row, and non-temporal partial-line writes
                     // measured slower here (366 -> 302 us at 2048 -> 2048,
                     // 14x14, batch 256).
-                    if (o < a.n) yb[int64_t(o) * a.y_c] = from_f32<TY>(epilogue<kEp>(a, o, acc[e][r]));
+                    if (o < a.n) yb[int64_t(o) * a.y_c] = from_f32<TY>(ep.apply(a, r, acc[e][r]));
                 }
             }
         }

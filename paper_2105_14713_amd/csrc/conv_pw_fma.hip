@@ -150,6 +150,27 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
     if (one_window && z1 > z0) stage(z0, z1 - z0);
 
     float* __restrict__ y = static_cast<float*>(a.y);
+    // Fused epilogue: the wave's N channels are the same for every tile of
+    // the run, so their scale and bias are read once here (inside the loop
+    // the compiler must reload them after each tile's stores, which may
+    // alias them, and every store would wait for those loads).
+    float eps[kEp ? N : 1], epb[kEp ? N : 1];
+    if constexpr (kEp) {
+#pragma unroll
+        for (int o = 0; o < N; ++o) {
+            const int32_t oc = g * N + o;
+            const bool in = g < a.G && oc < a.n;
+            // (wave-uniform: kept in scalar registers)
+            eps[o] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                         __builtin_bit_cast(int32_t, in && a.ep_scale ? a.ep_scale[oc] : 1.f)));
+            epb[o] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                         __builtin_bit_cast(int32_t, in && a.ep_bias ? a.ep_bias[oc] : 0.f)));
+        }
+    }
+    auto ep = [&](int o, float v) {
+        if constexpr (kEp) return epilogue_act(a, fmaf(v, eps[o], epb[o]));
+        else return v;
+    };
     for (int32_t tile = t0; tile < t1; ++tile) {
 #pragma unroll
         for (int i = 0; i < PPT; ++i) {
@@ -203,14 +224,13 @@ __global__ void __launch_bounds__(kFThreads) pw_fma(ConvArgs a) {
             if (oc >= a.n) continue;
             if constexpr (V4) {
                 if (yo[0] >= 0) {
-                    const f32x4 v = {epilogue<kEp>(a, oc, acc[o][0]), epilogue<kEp>(a, oc, acc[o][1]),
-                                     epilogue<kEp>(a, oc, acc[o][2]), epilogue<kEp>(a, oc, acc[o][3])};
+                    const f32x4 v = {ep(o, acc[o][0]), ep(o, acc[o][1]), ep(o, acc[o][2]), ep(o, acc[o][3])};
                     store_out(reinterpret_cast<f32x4*>(y + yo[0] + int64_t(oc) * a.y_c), v);
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < PPT; ++i)
-                    if (yo[i] >= 0) store_out(&y[yo[i] + int64_t(oc) * a.y_c], epilogue<kEp>(a, oc, acc[o][i]));
+                    if (yo[i] >= 0) store_out(&y[yo[i] + int64_t(oc) * a.y_c], ep(o, acc[o][i]));
             }
         }
     }

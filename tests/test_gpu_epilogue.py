@@ -26,6 +26,7 @@ def _gpu():
 KINDS = {
     "kxk": (3, 1, 1, 32, 40, torch.float32, 14, {}),
     "kxk_split_requested": (3, 1, 1, 32, 40, torch.float32, 14, {"kxk_split": 4, "kxk_tp": 128}),
+    "kxk_split_7x7": (3, 1, 1, 32, 40, torch.float32, 7, {"kxk_split": 4, "kxk_tp": 128}),
     "kxk_stem": (7, 2, 3, 32, 3, torch.float32, 30, {}),
     "tile": (1, 1, 0, 16, 200, torch.float32, 12, {"pw_kernel": 1}),
     "direct": (1, 2, 0, 32, 90, torch.float32, 12, {"pw_kernel": 3}),
