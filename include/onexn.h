@@ -198,7 +198,10 @@ onexn_status onexn_conv2d_fwd(const int32_t* P_dev, const int32_t* I_dev, const 
  * scale_dev, bias_dev: device fp32[n], or NULL for 1 and 0.  act: ONEXN_ACT_*.
  * Every other argument, the result layout and the errors are those of
  * onexn_conv2d_fwd (plus ARG for an unknown act); with NULL, NULL,
- * ONEXN_ACT_NONE the result equals onexn_conv2d_fwd's bit for bit.
+ * ONEXN_ACT_NONE the result equals onexn_conv2d_fwd's bit for bit.  A k x k
+ * layer whose output is at most 16 MB may run as the split convolution
+ * (fill, convolution) followed by a pass that applies the epilogue to y; a
+ * HIP error from that last launch may leave y holding the sums without it.
  */
 onexn_status onexn_conv2d_fwd_fused(const int32_t* P_dev, const int32_t* I_dev, const void* D_dev,
                                     onexn_dtype wdt, int32_t n, int32_t m, int32_t kh, int32_t kw,
